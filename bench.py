@@ -1,0 +1,222 @@
+"""Throughput of the CNN forward pass on one MI355X.
+
+One step is one cnn_net_fwd over a batch of synthetic images: the whole
+network, every layer in the paper's layer-setup order (Sec. 4), parameters
+resident in HBM, input already on the device (the paper also excludes
+parameter loading from its timings, Sec. 4).  Default workload: the
+AlexNet-shaped network at batch 64.
+
+Prints ONE JSON line: images/s (whole job), per-layer times measured with
+HIP events recorded between the layers of every timed step, the convolution
+rate as a fraction of the fp32 matrix-core peak, a roofline entry for the
+dominant kernel, and the CPU oracle's rate on a bounded sample of the same
+workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "images/sec + conv GFLOP/s (% fp32 MFMA peak), AlexNet-shaped fp32 batch 64"
+PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
+PEAK_HBM_GBS = 8000.0           # MI355X HBM3E
+
+
+def layer_work(net, batch, cnn):
+    """Per layer: (name, kind, flops, bytes, kernel) with algorithmic counts.
+
+    conv: 2*N*K*P*Q*(C/G)*R*S flops; fc: 2*N*I*O flops; pool: read input +
+    write output (+ int32 index); LRN: read + write; ReLU: read + write.
+    Bytes are fp32 tensor sizes; parameters are counted for conv / fc only as
+    part of the contraction, not as bandwidth."""
+    c, h, w = net.input_chw
+    out = []
+    counts = {}
+    for layer in net.layers:
+        counts[layer.kind] = counts.get(layer.kind, 0) + 1
+        name = f"{layer.kind}{counts[layer.kind]}"
+        if layer.kind == "conv":
+            p, q = cnn.cnn_conv2d_out_shape(h, w, *layer.kernel, layer.stride, layer.pad)
+            k = layer.out_channels
+            flops = 2 * batch * k * p * q * (c // layer.groups) * layer.kernel[0] * layer.kernel[1]
+            byts = 4 * batch * (c * h * w + k * p * q)
+            out.append((name, "conv", flops, byts))
+            c, h, w = k, p, q
+        elif layer.kind == "fc":
+            i, o = c * h * w, layer.out_features
+            out.append((name, "fc", 2 * batch * i * o, 4 * (batch * (i + o) + i * o)))
+            c, h, w = o, 1, 1
+        elif layer.kind == "pool":
+            p, q = cnn.cnn_pool_out_shape(h, w, layer.kernel, layer.stride, layer.pad, layer.ceil)
+            byts = 4 * batch * c * (h * w + p * q)
+            out.append((name, "pool", 0, byts))
+            h, w = p, q
+        elif layer.kind == "lrn":
+            out.append((name, "lrn", 0, 8 * batch * c * h * w))
+        else:
+            out.append((name, "relu", 0, 8 * batch * c * h * w))
+    return out
+
+
+def source_digest():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1511_07376_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload, layer_name):
+    """HBM bytes per launch measured by rocprofv3 --pmc (FETCH_SIZE, WRITE_SIZE),
+    kept with the digest of the kernel sources they were taken on; None when the
+    sources have changed since."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_digest") != source_digest():
+        return None
+    lay = rec.get("layers", {}).get(layer_name)
+    return None if lay is None else lay.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(net, x, params, budget_s):
+    import oracle
+    threads = oracle.get_threads()
+    t0 = time.perf_counter()
+    oracle.net_fwd(net, x[:1], params)
+    t1 = time.perf_counter() - t0
+    n_more = int(max(0, min(x.shape[0] - 1, (budget_s - t1) / max(t1, 1e-3))))
+    t2 = 0.0
+    if n_more > 0:
+        t0 = time.perf_counter()
+        oracle.net_fwd(net, x[1:1 + n_more], params)
+        t2 = time.perf_counter() - t0
+    n = 1 + n_more
+    return {"value": n / (t1 + t2), "unit": "images/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} of the {x.shape[0]} images of the same batch through the oracle's "
+                      f"layer-by-layer network (double accumulation, OpenMP over images x "
+                      f"channels), {t1 + t2:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--net", default="alexnet", choices=["lenet", "cifar_quick", "alexnet"])
+    ap.add_argument("--batch", type=int, default=None)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle work for the CPU baseline (0 disables it)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
+              "(the images of a batch are independent: on N GPUs each would run batch/N)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1511_07376_amd import cnn
+    from paper_1511_07376_amd import workloads as wl
+
+    net = wl.NETS[args.net]
+    batch = args.batch or (64 if args.net == "alexnet" else net.default_batch)
+    x = wl.make_input(net, batch, args.seed)
+    params = wl.make_params(net, args.seed)
+    model = cnn.Network(net, params)
+    xd = torch.from_numpy(x).cuda()
+    yd = torch.empty(model.out_shape(batch), device="cuda")
+
+    nl = len(net.layers)
+    for _ in range(args.warmup):
+        model(xd, y=yd)
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(nl + 1)] for _ in range(args.steps)]
+    for evs in events:
+        for e in evs:
+            e.record()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for k in range(args.steps):
+        model(xd, y=yd, events=events[k])
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / args.steps
+    assert torch.isfinite(yd).all().item(), "non-finite output"
+
+    layer_ms = [float(np.mean([events[k][i].elapsed_time(events[k][i + 1]) for k in range(args.steps)]))
+                for i in range(nl)]
+    work = layer_work(net, batch, cnn)
+    layers = []
+    for (name, kind, flops, byts), ms in zip(work, layer_ms):
+        ent = {"layer": name, "ms": round(ms, 5)}
+        if kind in ("conv", "fc"):
+            tf = flops / (ms * 1e-3) / 1e12 if ms > 0 else 0.0
+            ent.update({"gflop": round(flops / 1e9, 4), "tflops": round(tf, 2),
+                        "frac_fp32_mfma": round(tf / PEAK_FP32_MFMA_TFLOPS, 4)})
+        else:
+            gbs = byts / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
+            ent.update({"mbytes": round(byts / 1e6, 2), "gbs": round(gbs, 1),
+                        "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
+        layers.append(ent)
+
+    conv_flops = sum(w[2] for w in work if w[1] == "conv")
+    conv_ms = sum(ms for w, ms in zip(work, layer_ms) if w[1] == "conv")
+    conv_tf = conv_flops / (conv_ms * 1e-3) / 1e12
+
+    dom = int(np.argmax(layer_ms))
+    dname, dkind, dflops, dbytes = work[dom]
+    workload = f"{net.name}_b{batch}"
+    if dkind in ("conv", "fc"):
+        ach = dflops / (layer_ms[dom] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_FP32_MFMA_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / PEAK_FP32_MFMA_TFLOPS, 4)}
+    else:
+        ach = dbytes / (layer_ms[dom] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / PEAK_HBM_GBS, 4)}
+    roof["traffic"] = stored_traffic(workload, dname)
+    roof["layer"] = dname
+    roof["launch_ms"] = round(layer_ms[dom], 5)
+
+    shape = "x".join(map(str, net.input_chw))
+    result = {
+        "metric": METRIC,
+        "value": round(batch / (ms_step * 1e-3), 1),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded uniform [0,1) images, N(0, std) weights and biases)",
+        "config": {"workload": f"{net.name}-shaped fp32 forward, batch {batch} x {shape}",
+                   "net": net.name, "batch": batch, "layers": nl},
+        "conv_gflops": round(conv_tf * 1e3, 1),
+        "conv_frac_fp32_mfma_peak": round(conv_tf / PEAK_FP32_MFMA_TFLOPS, 4),
+        "conv_ms": round(conv_ms, 5),
+        "layers": layers,
+        "roofline": roof,
+    }
+    if args.cpu_budget > 0:
+        result["cpu_baseline"] = cpu_baseline(net, x, params, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,186 @@
+/*
+ * cnn.h -- C ABI of libcnn, the gfx950 (MI355X) forward pass of trained CNNs.
+ *
+ * The layer set is the one the paper's library executes: convolution, max and
+ * mean pooling, fully connected, ReLU and local response normalization
+ * (Sec. 3.1), chained into networks that run on one image or a batch
+ * (Sec. 3.3, the compute() call), with ReLU embedded into the preceding
+ * layer (Sec. 3.5).  The paper gives no formulas; each entry point states
+ * the definition it computes.
+ *
+ * Conventions for every entry point:
+ *  - Tensors are fp32, NCHW, row-major, contiguous, in DEVICE memory,
+ *    allocated and owned by the caller.  The library allocates nothing.
+ *  - Calls are asynchronous: argument checks run on the host first and a
+ *    negative status means nothing was enqueued; on CNN_OK the kernels are
+ *    enqueued on `stream` (a hipStream_t; NULL = the null stream) and the
+ *    caller synchronises.
+ *  - Input and output buffers must not overlap, except that cnn_relu_fwd
+ *    allows y == x.
+ *  - No exception or abort crosses the ABI.  cnn_last_error() returns a
+ *    thread-local message describing the last non-OK status of this thread.
+ *  - Sizes are int (each tensor must hold fewer than 2^31 elements).
+ */
+#ifndef CNN_H
+#define CNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum cnn_status {
+    CNN_OK = 0,
+    CNN_ERR_INVALID = -1,     /* bad argument: null pointer, bad size, inconsistent shapes */
+    CNN_ERR_UNSUPPORTED = -2, /* well-formed but outside what the kernels implement */
+    CNN_ERR_HIP = -3,         /* the HIP runtime reported an error at launch */
+    CNN_ERR_WORKSPACE = -4    /* workspace missing or smaller than required */
+} cnn_status;
+
+typedef void* cnn_stream_t; /* hipStream_t */
+
+/* Convolution output size, floor rule: P = (H + 2*ph - R) / sh + 1,
+ * Q = (W + 2*pw - S) / sw + 1.  Requires H + 2*ph >= R, W + 2*pw >= S,
+ * strides >= 1, pads >= 0. */
+int cnn_conv2d_out_shape(int H, int W, int R, int S, int sh, int sw,
+                         int ph, int pw, int* P, int* Q);
+
+/* Pooling output size.  ceil_mode = 1: P = ceil((H + 2*ph - kh) / sh) + 1,
+ * then one less if that last window would start at or past H + ph (so that
+ * every window overlaps the image); ceil_mode = 0: floor instead of ceil.
+ * Requires 0 <= ph < kh and 0 <= pw < kw. */
+int cnn_pool_out_shape(int H, int W, int kh, int kw, int sh, int sw,
+                       int ph, int pw, int ceil_mode, int* P, int* Q);
+
+/* Convolution layer (Sec. 3.1; computed on the GPU, Sec. 3.5): grouped 2-D
+ * cross-correlation (no kernel flip) with stride, zero padding and bias,
+ *   y[n,k,p,q] = b[k] + sum_{c < C/G, r < R, s < S}
+ *                x[n, g*C/G + c, p*sh - ph + r, q*sw - pw + s] * w[k,c,r,s]
+ * where g = k / (K/G) and x is zero outside the image.
+ *   x    [N][C][H][W]      w [K][C/G][R][S]      bias [K] or NULL
+ *   y    [N][K][P][Q]      (P, Q from cnn_conv2d_out_shape)
+ * groups must divide C and K.  fuse_relu = 1 applies y = max(y, 0) in the
+ * same kernel (a Conv+ReLU layer).  Errors: CNN_ERR_INVALID for null x/w/y,
+ * non-positive sizes or bad shapes. */
+int cnn_conv2d_fwd(const float* x, int N, int C, int H, int W,
+                   const float* w, int K, int R, int S, const float* bias,
+                   int sh, int sw, int ph, int pw, int groups, int fuse_relu,
+                   float* y, cnn_stream_t stream);
+
+/* Fully-connected layer (Sec. 3.1; a matrix-vector product per image,
+ * Sec. 3.5): y[n,o] = b[o] + sum_i x[n,i] * w[o,i].
+ *   x [N][I] (an NCHW tensor flattened: i = c*H*W + h*W + w)
+ *   w [O][I]   bias [O] or NULL   y [N][O]
+ * fuse_relu = 1 applies y = max(y, 0) (an FC+ReLU layer).  For N >= 1 the
+ * result is the same for every batch split; when the reduction is split
+ * across workgroups the summation order is not fixed run to run. */
+int cnn_fc_fwd(const float* x, int N, int I, const float* w,
+               const float* bias, int O, int fuse_relu, float* y,
+               cnn_stream_t stream);
+
+typedef enum cnn_pool_mode { CNN_POOL_MAX = 0, CNN_POOL_AVG = 1 } cnn_pool_mode;
+
+/* Max / mean pooling layer (Sec. 3.1).  Window (p, q) covers rows
+ * [p*sh - ph, p*sh - ph + kh) and columns [q*sw - pw, q*sw - pw + kw),
+ * clipped to the image.
+ *   MAX: y = the largest element; idx (optional, int32 [N][C][P][Q]) receives
+ *        h*W + w of the FIRST largest element in row-major order.
+ *   AVG: y = (sum of the clipped window) / (window area clipped to the padded
+ *        extent [-ph, H + ph) x [-pw, W + pw)).
+ * fuse_relu = 1 applies y = max(y, 0) after pooling (a Pooling+ReLU layer);
+ * the index stays that of the pre-ReLU maximum.  idx must be NULL for AVG.
+ * Inputs must be finite (NaN ordering is not defined). */
+int cnn_pool_fwd(const float* x, int N, int C, int H, int W, int mode,
+                 int kh, int kw, int sh, int sw, int ph, int pw, int ceil_mode,
+                 int fuse_relu, float* y, int32_t* idx, cnn_stream_t stream);
+
+/* Local response normalization across channels (Sec. 3.1; AlexNet rows of
+ * the layer-setup table, Sec. 4):
+ *   y[n,c,h,w] = x[n,c,h,w] * (k + alpha/size * sum_{c'} x[n,c',h,w]^2)^(-beta)
+ * with c' over [c - size/2, c + size/2] clipped to [0, C).  size must be odd
+ * (CNN_ERR_UNSUPPORTED otherwise). */
+int cnn_lrn_fwd(const float* x, int N, int C, int H, int W, int size,
+                float alpha, float beta, float k, float* y, cnn_stream_t stream);
+
+/* ReLU layer (Sec. 3.1): y[i] = x[i] > 0 ? x[i] : +0.0f for i < n.
+ * y == x (in place) is allowed. */
+int cnn_relu_fwd(const float* x, float* y, int64_t n, cnn_stream_t stream);
+
+/* ---------------------------------------------------------------- networks
+ * A network is an array of layer descriptors executed in order (the paper's
+ * NetFile layer list, Sec. 3.2, and compute(), Sec. 3.3).  Parameters are
+ * caller-owned device buffers that stay resident between calls.
+ */
+typedef enum cnn_layer_type {
+    CNN_LAYER_CONV = 0,
+    CNN_LAYER_FC = 1,
+    CNN_LAYER_POOL = 2,
+    CNN_LAYER_LRN = 3,
+    CNN_LAYER_RELU = 4
+} cnn_layer_type;
+
+typedef struct cnn_layer_desc {
+    int32_t type;          /* cnn_layer_type */
+    int32_t out_channels;  /* CONV: K; FC: O */
+    int32_t kernel_h;      /* CONV: R; POOL: kh */
+    int32_t kernel_w;      /* CONV: S; POOL: kw */
+    int32_t stride_h;      /* CONV, POOL */
+    int32_t stride_w;
+    int32_t pad_h;         /* CONV, POOL */
+    int32_t pad_w;
+    int32_t groups;        /* CONV (>= 1) */
+    int32_t pool_mode;     /* POOL: cnn_pool_mode */
+    int32_t ceil_mode;     /* POOL */
+    int32_t fuse_relu;     /* CONV, FC, POOL: ReLU after the layer */
+    int32_t lrn_size;      /* LRN */
+    float lrn_alpha;       /* LRN */
+    float lrn_beta;        /* LRN */
+    float lrn_k;           /* LRN */
+    int32_t in_channels;   /* CONV: expected input channels C (0 = not checked) */
+    int32_t in_features;   /* FC: expected C*H*W of its input (0 = not checked) */
+    const float* weight;   /* CONV: [K][C/G][R][S]; FC: [O][I] */
+    const float* bias;     /* CONV: [K]; FC: [O]; or NULL */
+    int32_t* pool_index;   /* POOL MAX: optional int32 [N][C][P][Q] output */
+} cnn_layer_desc;
+
+/* Output shape of the network for an N x C x H x W input (outC x outH x outW
+ * per image; FC layers give outH = outW = 1).  CNN_ERR_INVALID /
+ * CNN_ERR_UNSUPPORTED describe the first bad layer. */
+int cnn_net_out_shape(const cnn_layer_desc* layers, int n_layers, int N, int C,
+                      int H, int W, int* outC, int* outH, int* outW);
+
+/* Device workspace cnn_net_fwd needs for this input: two activation buffers
+ * of the largest intermediate tensor, each 256-byte aligned.  0 on error. */
+size_t cnn_net_workspace_bytes(const cnn_layer_desc* layers, int n_layers,
+                               int N, int C, int H, int W);
+
+/* Runs the network on x [N][C][H][W] and writes the last layer's output to y
+ * ([N][outC][outH][outW]).  ws is caller-owned device memory of at least
+ * cnn_net_workspace_bytes(); intermediates live there.  A RELU layer that
+ * follows a CONV, FC or POOL layer is executed inside that layer (Sec. 3.5).
+ * Every layer is validated before the first launch. */
+int cnn_net_fwd(const cnn_layer_desc* layers, int n_layers, const float* x,
+                int N, int C, int H, int W, float* y, void* ws, size_t ws_bytes,
+                cnn_stream_t stream);
+
+/* As cnn_net_fwd, and records events[i] (hipEvent_t) on the stream before
+ * layer i and events[n_layers] after the last one, so that the caller can
+ * time each layer (the paper times whole networks and the heaviest conv
+ * layer separately, Sec. 4.2).  A RELU layer executed inside its predecessor
+ * gets an empty interval. */
+int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x,
+                      int N, int C, int H, int W, float* y, void* ws,
+                      size_t ws_bytes, void* const* events, cnn_stream_t stream);
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char* cnn_last_error(void);
+
+/* Library version string. */
+const char* cnn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CNN_H */

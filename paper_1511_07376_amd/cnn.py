@@ -1,0 +1,325 @@
+"""Python binding of libcnn (include/cnn.h): argument marshalling only.
+
+Every function here checks that its tensors are contiguous float32 CUDA
+(ROCm) tensors, passes their device pointers and the current torch stream to
+the C entry point of the same name, and raises ``CnnError`` with
+``cnn_last_error()`` on a non-OK status.  All computation happens in the HIP
+kernels of libcnn; torch provides device memory and the stream.  Importing
+this module fails if libcnn.so has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence, Tuple
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libcnn.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python __graft_entry__.py` "
+                      "(or paper_1511_07376_amd/build.py) before using the GPU path")
+
+lib = ctypes.CDLL(LIB_PATH)
+
+_i = ctypes.c_int
+_p = ctypes.c_void_p
+_ip = ctypes.POINTER(ctypes.c_int)
+
+CNN_OK, CNN_ERR_INVALID, CNN_ERR_UNSUPPORTED, CNN_ERR_HIP, CNN_ERR_WORKSPACE = 0, -1, -2, -3, -4
+CNN_POOL_MAX, CNN_POOL_AVG = 0, 1
+CNN_LAYER_CONV, CNN_LAYER_FC, CNN_LAYER_POOL, CNN_LAYER_LRN, CNN_LAYER_RELU = 0, 1, 2, 3, 4
+
+
+class cnn_layer_desc(ctypes.Structure):
+    _fields_ = [
+        ("type", ctypes.c_int32), ("out_channels", ctypes.c_int32),
+        ("kernel_h", ctypes.c_int32), ("kernel_w", ctypes.c_int32),
+        ("stride_h", ctypes.c_int32), ("stride_w", ctypes.c_int32),
+        ("pad_h", ctypes.c_int32), ("pad_w", ctypes.c_int32),
+        ("groups", ctypes.c_int32), ("pool_mode", ctypes.c_int32),
+        ("ceil_mode", ctypes.c_int32), ("fuse_relu", ctypes.c_int32),
+        ("lrn_size", ctypes.c_int32), ("lrn_alpha", ctypes.c_float),
+        ("lrn_beta", ctypes.c_float), ("lrn_k", ctypes.c_float),
+        ("in_channels", ctypes.c_int32), ("in_features", ctypes.c_int32),
+        ("weight", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("pool_index", ctypes.c_void_p),
+    ]
+
+
+lib.cnn_conv2d_out_shape.argtypes = [_i] * 8 + [_ip, _ip]
+lib.cnn_pool_out_shape.argtypes = [_i] * 9 + [_ip, _ip]
+lib.cnn_conv2d_fwd.argtypes = [_p, _i, _i, _i, _i, _p, _i, _i, _i, _p, _i, _i, _i, _i, _i, _i, _p, _p]
+lib.cnn_fc_fwd.argtypes = [_p, _i, _i, _p, _p, _i, _i, _p, _p]
+lib.cnn_pool_fwd.argtypes = [_p, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p]
+lib.cnn_lrn_fwd.argtypes = [_p, _i, _i, _i, _i, _i, ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                            _p, _p]
+lib.cnn_relu_fwd.argtypes = [_p, _p, ctypes.c_int64, _p]
+_descp = ctypes.POINTER(cnn_layer_desc)
+lib.cnn_net_out_shape.argtypes = [_descp, _i, _i, _i, _i, _i, _ip, _ip, _ip]
+lib.cnn_net_workspace_bytes.argtypes = [_descp, _i, _i, _i, _i, _i]
+lib.cnn_net_workspace_bytes.restype = ctypes.c_size_t
+lib.cnn_net_fwd.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t, _p]
+lib.cnn_net_fwd_timed.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
+                                  ctypes.POINTER(ctypes.c_void_p), _p]
+lib.cnn_last_error.restype = ctypes.c_char_p
+lib.cnn_version.restype = ctypes.c_char_p
+for _name in ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
+              "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_net_out_shape", "cnn_net_fwd",
+              "cnn_net_fwd_timed"):
+    getattr(lib, _name).restype = _i
+
+EXPORTED = ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
+            "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_net_out_shape",
+            "cnn_net_workspace_bytes", "cnn_net_fwd", "cnn_net_fwd_timed", "cnn_last_error",
+            "cnn_version")
+
+
+class CnnError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"libcnn status {status}: {message}")
+        self.status = status
+
+
+def cnn_last_error() -> str:
+    return lib.cnn_last_error().decode()
+
+
+def cnn_version() -> str:
+    return lib.cnn_version().decode()
+
+
+def _ok(rc: int) -> None:
+    if rc != CNN_OK:
+        raise CnnError(rc, cnn_last_error())
+
+
+def _dev(t: Optional[torch.Tensor], name: str, dtype=torch.float32):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise TypeError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _pair(v) -> Tuple[int, int]:
+    return (int(v), int(v)) if isinstance(v, int) else (int(v[0]), int(v[1]))
+
+
+def cnn_conv2d_out_shape(H, W, R, S, stride=1, pad=0) -> Tuple[int, int]:
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    P, Q = ctypes.c_int(), ctypes.c_int()
+    _ok(lib.cnn_conv2d_out_shape(H, W, R, S, sh, sw, ph, pw, ctypes.byref(P), ctypes.byref(Q)))
+    return P.value, Q.value
+
+
+def cnn_pool_out_shape(H, W, kernel, stride, pad=0, ceil_mode=True) -> Tuple[int, int]:
+    kh, kw = _pair(kernel)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    P, Q = ctypes.c_int(), ctypes.c_int()
+    _ok(lib.cnn_pool_out_shape(H, W, kh, kw, sh, sw, ph, pw, int(ceil_mode), ctypes.byref(P),
+                               ctypes.byref(Q)))
+    return P.value, Q.value
+
+
+def cnn_conv2d_fwd(x, w, bias=None, stride=1, pad=0, groups=1, fuse_relu=False, y=None, stream=None):
+    """x [N][C][H][W], w [K][C/G][R][S], bias [K] -> y [N][K][P][Q] (allocated if None)."""
+    N, C, H, W = x.shape
+    K, _cg, R, S = w.shape
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    if y is None:
+        P, Q = cnn_conv2d_out_shape(H, W, R, S, (sh, sw), (ph, pw))
+        y = torch.empty((N, K, P, Q), dtype=torch.float32, device=x.device)
+    _ok(lib.cnn_conv2d_fwd(_dev(x, "x"), N, C, H, W, _dev(w, "w"), K, R, S, _dev(bias, "bias"),
+                           sh, sw, ph, pw, groups, int(fuse_relu), _dev(y, "y"), _stream(stream)))
+    return y
+
+
+def cnn_fc_fwd(x, w, bias=None, fuse_relu=False, y=None, stream=None):
+    """x [N][I] (or [N][C][H][W], read flattened), w [O][I] -> y [N][O]."""
+    N = x.shape[0]
+    I = x.numel() // max(N, 1) if N else int(w.shape[1])
+    O = w.shape[0]
+    if y is None:
+        y = torch.empty((N, O), dtype=torch.float32, device=x.device)
+    _ok(lib.cnn_fc_fwd(_dev(x, "x"), N, I, _dev(w, "w"), _dev(bias, "bias"), O, int(fuse_relu),
+                       _dev(y, "y"), _stream(stream)))
+    return y
+
+
+def cnn_pool_fwd(x, mode="max", kernel=2, stride=2, pad=0, ceil_mode=True, fuse_relu=False,
+                 with_index=False, y=None, idx=None, stream=None):
+    """Returns y, or (y, idx) for max pooling with with_index."""
+    N, C, H, W = x.shape
+    kh, kw = _pair(kernel)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    m = {"max": CNN_POOL_MAX, "avg": CNN_POOL_AVG}[mode] if isinstance(mode, str) else int(mode)
+    P, Q = cnn_pool_out_shape(H, W, (kh, kw), (sh, sw), (ph, pw), ceil_mode)
+    if y is None:
+        y = torch.empty((N, C, P, Q), dtype=torch.float32, device=x.device)
+    if with_index and idx is None:
+        idx = torch.empty((N, C, P, Q), dtype=torch.int32, device=x.device)
+    _ok(lib.cnn_pool_fwd(_dev(x, "x"), N, C, H, W, m, kh, kw, sh, sw, ph, pw, int(ceil_mode),
+                         int(fuse_relu), _dev(y, "y"), _dev(idx, "idx", torch.int32), _stream(stream)))
+    return (y, idx) if idx is not None else y
+
+
+def cnn_lrn_fwd(x, size=5, alpha=1e-4, beta=0.75, k=1.0, y=None, stream=None):
+    N, C, H, W = x.shape
+    if y is None:
+        y = torch.empty_like(x)
+    _ok(lib.cnn_lrn_fwd(_dev(x, "x"), N, C, H, W, size, alpha, beta, k, _dev(y, "y"), _stream(stream)))
+    return y
+
+
+def cnn_relu_fwd(x, y=None, stream=None):
+    """y = max(x, 0); pass y=x for in place."""
+    if y is None:
+        y = torch.empty_like(x)
+    if y.numel() != x.numel():
+        raise ValueError("relu: x and y differ in size")
+    _ok(lib.cnn_relu_fwd(_dev(x, "x"), _dev(y, "y"), x.numel(), _stream(stream)))
+    return y
+
+
+# ---------------------------------------------------------------- networks
+class Network:
+    """A layer-descriptor array bound to device-resident parameters.
+
+    Built from a ``workloads.Net`` and its (weight, bias) list; parameters are
+    copied to the device once (loading is outside the timed path, as in the
+    paper's measurements).  ``pool_index=True`` allocates an int32 index
+    output for every max-pooling layer (per batch size, on first use).
+    """
+
+    def __init__(self, net, params, device="cuda", pool_index: bool = False):
+        self.net = net
+        self.device = torch.device(device)
+        self.weights: List[Tuple[Optional[torch.Tensor], Optional[torch.Tensor]]] = []
+        for layer, pr in zip(net.layers, params):
+            if layer.has_params:
+                self.weights.append((torch.from_numpy(pr[0]).to(self.device).contiguous(),
+                                     torch.from_numpy(pr[1]).to(self.device).contiguous()))
+            else:
+                self.weights.append((None, None))
+        self.pool_index = pool_index
+        self.indices: List[Optional[torch.Tensor]] = [None] * len(net.layers)
+        self.descs = (cnn_layer_desc * len(net.layers))()
+        for i, (layer, (w, b)) in enumerate(zip(net.layers, self.weights)):
+            d = self.descs[i]
+            if layer.kind == "conv":
+                d.type = CNN_LAYER_CONV
+                d.in_channels = layer.in_channels
+                d.out_channels = layer.out_channels
+                d.kernel_h, d.kernel_w = layer.kernel
+                d.stride_h, d.stride_w = layer.stride
+                d.pad_h, d.pad_w = layer.pad
+                d.groups = layer.groups
+                d.fuse_relu = int(layer.relu)
+            elif layer.kind == "fc":
+                d.type = CNN_LAYER_FC
+                d.out_channels = layer.out_features
+                d.in_features = layer.in_features
+                d.fuse_relu = int(layer.relu)
+            elif layer.kind == "pool":
+                d.type = CNN_LAYER_POOL
+                d.pool_mode = CNN_POOL_MAX if layer.mode == "max" else CNN_POOL_AVG
+                d.kernel_h, d.kernel_w = layer.kernel
+                d.stride_h, d.stride_w = layer.stride
+                d.pad_h, d.pad_w = layer.pad
+                d.ceil_mode = int(layer.ceil)
+                d.fuse_relu = int(layer.relu)
+            elif layer.kind == "lrn":
+                d.type = CNN_LAYER_LRN
+                d.lrn_size = layer.size
+                d.lrn_alpha, d.lrn_beta, d.lrn_k = layer.alpha, layer.beta, layer.k
+            elif layer.kind == "relu":
+                d.type = CNN_LAYER_RELU
+            else:
+                raise ValueError(f"unknown layer kind {layer.kind}")
+            d.weight = w.data_ptr() if w is not None else None
+            d.bias = b.data_ptr() if b is not None else None
+        self._ws: Optional[torch.Tensor] = None
+        self._ws_key = None
+
+    def out_shape(self, N: int) -> Tuple[int, int, int, int]:
+        C, H, W = self.net.input_chw
+        oc, oh, ow = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+        _ok(lib.cnn_net_out_shape(self.descs, len(self.descs), N, C, H, W, ctypes.byref(oc),
+                                  ctypes.byref(oh), ctypes.byref(ow)))
+        if self.net.layers[-1].kind == "fc":
+            return (N, oc.value)
+        return (N, oc.value, oh.value, ow.value)
+
+    def workspace_bytes(self, N: int) -> int:
+        C, H, W = self.net.input_chw
+        n = lib.cnn_net_workspace_bytes(self.descs, len(self.descs), N, C, H, W)
+        if n == 0 and N > 0:
+            raise CnnError(CNN_ERR_INVALID, cnn_last_error())
+        return int(n)
+
+    def _prepare(self, N: int):
+        key = N
+        if self._ws_key != key:
+            nbytes = self.workspace_bytes(N)
+            self._ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+            self._ws_key = key
+            if self.pool_index:
+                self._alloc_indices(N)
+
+    def _alloc_indices(self, N: int):
+        C, H, W = self.net.input_chw
+        c, h, w = C, H, W
+        for i, layer in enumerate(self.net.layers):
+            if layer.kind == "conv":
+                h, w = cnn_conv2d_out_shape(h, w, *layer.kernel, layer.stride, layer.pad)
+                c = layer.out_channels
+            elif layer.kind == "pool":
+                h, w = cnn_pool_out_shape(h, w, layer.kernel, layer.stride, layer.pad, layer.ceil)
+                if layer.mode == "max":
+                    self.indices[i] = torch.empty((N, c, h, w), dtype=torch.int32, device=self.device)
+                    self.descs[i].pool_index = self.indices[i].data_ptr()
+            elif layer.kind == "fc":
+                c, h, w = layer.out_features, 1, 1
+
+    def forward(self, x: torch.Tensor, y: Optional[torch.Tensor] = None, stream=None,
+                events: Optional[Sequence] = None) -> torch.Tensor:
+        """cnn_net_fwd (or cnn_net_fwd_timed with one torch.cuda.Event per layer + 1)."""
+        N, C, H, W = x.shape
+        self._prepare(N)
+        if y is None:
+            y = torch.empty(self.out_shape(N), dtype=torch.float32, device=x.device)
+        args = (self.descs, len(self.descs), _dev(x, "x"), N, C, H, W, _dev(y, "y"),
+                self._ws.data_ptr(), self._ws.numel())
+        if events is None:
+            _ok(lib.cnn_net_fwd(*args, _stream(stream)))
+        else:
+            if len(events) != len(self.descs) + 1:
+                raise ValueError("need one event per layer plus one")
+            arr = (ctypes.c_void_p * len(events))(*[e.cuda_event if hasattr(e, "cuda_event") else int(e)
+                                                    for e in events])
+            _ok(lib.cnn_net_fwd_timed(*args, arr, _stream(stream)))
+        return y
+
+    __call__ = forward
+
+
+def cnn_net_fwd(network: Network, x, y=None, stream=None):
+    return network.forward(x, y, stream)

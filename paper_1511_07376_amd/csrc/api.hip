@@ -1,0 +1,382 @@
+// libcnn C ABI: argument validation, dispatch to the kernels, and the network
+// executor (a layer list run in order over two ping-pong activation buffers
+// in a caller-provided workspace).
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+namespace cnn {
+
+namespace {
+thread_local char g_err[512] = "";
+}
+
+int fail(int status, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int check_launch(const char* what) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(CNN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return CNN_OK;
+}
+
+int conv_out(int H, int W, int R, int S, int sh, int sw, int ph, int pw, int* P, int* Q) {
+    if (H <= 0 || W <= 0) return fail(CNN_ERR_INVALID, "conv: input %dx%d is empty", H, W);
+    if (R <= 0 || S <= 0) return fail(CNN_ERR_INVALID, "conv: kernel %dx%d", R, S);
+    if (sh <= 0 || sw <= 0) return fail(CNN_ERR_INVALID, "conv: stride %dx%d", sh, sw);
+    if (ph < 0 || pw < 0) return fail(CNN_ERR_INVALID, "conv: negative padding");
+    if (H + 2 * ph < R || W + 2 * pw < S)
+        return fail(CNN_ERR_INVALID, "conv: kernel %dx%d larger than padded input %dx%d", R, S,
+                    H + 2 * ph, W + 2 * pw);
+    *P = (H + 2 * ph - R) / sh + 1;
+    *Q = (W + 2 * pw - S) / sw + 1;
+    return CNN_OK;
+}
+
+namespace {
+int pool_extent(int in, int k, int s, int pad, int ceil_mode) {
+    const int span = in + 2 * pad - k;
+    int out = ceil_mode ? (span + s - 1) / s + 1 : span / s + 1;
+    if (ceil_mode && (out - 1) * s >= in + pad) --out;  // window would start past the image
+    return out;
+}
+}  // namespace
+
+int pool_out(int H, int W, int kh, int kw, int sh, int sw, int ph, int pw, int ceil_mode, int* P,
+             int* Q) {
+    if (H <= 0 || W <= 0) return fail(CNN_ERR_INVALID, "pool: input %dx%d is empty", H, W);
+    if (kh <= 0 || kw <= 0) return fail(CNN_ERR_INVALID, "pool: window %dx%d", kh, kw);
+    if (sh <= 0 || sw <= 0) return fail(CNN_ERR_INVALID, "pool: stride %dx%d", sh, sw);
+    if (ph < 0 || pw < 0 || ph >= kh || pw >= kw)
+        return fail(CNN_ERR_INVALID, "pool: padding %dx%d must be >= 0 and below the window %dx%d",
+                    ph, pw, kh, kw);
+    if (H + 2 * ph < kh || W + 2 * pw < kw)
+        return fail(CNN_ERR_INVALID, "pool: window larger than padded input");
+    *P = pool_extent(H, kh, sh, ph, ceil_mode);
+    *Q = pool_extent(W, kw, sw, pw, ceil_mode);
+    return CNN_OK;
+}
+
+namespace {
+
+bool too_big(int64_t a, int64_t b, int64_t c = 1, int64_t d = 1) {
+    // product of non-negative factors above the int32 element limit
+    int64_t v = a;
+    for (int64_t f : {b, c, d}) {
+        if (f != 0 && v > kMaxElems / f) return true;
+        v *= f;
+    }
+    return v > kMaxElems;
+}
+
+int check_conv(int N, int C, int H, int W, int K, int R, int S, int sh, int sw, int ph, int pw,
+               int groups, ConvShape* s) {
+    if (N < 0) return fail(CNN_ERR_INVALID, "conv: batch %d", N);
+    if (C <= 0 || K <= 0) return fail(CNN_ERR_INVALID, "conv: channels C=%d K=%d", C, K);
+    if (groups <= 0 || C % groups || K % groups)
+        return fail(CNN_ERR_INVALID, "conv: groups=%d must divide C=%d and K=%d", groups, C, K);
+    int P, Q;
+    int rc = conv_out(H, W, R, S, sh, sw, ph, pw, &P, &Q);
+    if (rc) return rc;
+    if (too_big(N, C, H, W) || too_big(N, K, P, Q) || too_big(K, C / groups, R, S))
+        return fail(CNN_ERR_UNSUPPORTED, "conv: a tensor exceeds 2^31-1 elements");
+    *s = ConvShape{N, C, H, W, K, R, S, sh, sw, ph, pw, groups, P, Q};
+    return CNN_OK;
+}
+
+int check_pool(int N, int C, int H, int W, int mode, int kh, int kw, int sh, int sw, int ph,
+               int pw, int ceil_mode, PoolShape* s) {
+    if (N < 0 || C <= 0) return fail(CNN_ERR_INVALID, "pool: N=%d C=%d", N, C);
+    if (mode != CNN_POOL_MAX && mode != CNN_POOL_AVG)
+        return fail(CNN_ERR_INVALID, "pool: mode %d", mode);
+    int P, Q;
+    int rc = pool_out(H, W, kh, kw, sh, sw, ph, pw, ceil_mode, &P, &Q);
+    if (rc) return rc;
+    if (too_big(N, C, H, W)) return fail(CNN_ERR_UNSUPPORTED, "pool: tensor exceeds 2^31-1 elements");
+    *s = PoolShape{N, C, H, W, kh, kw, sh, sw, ph, pw, P, Q};
+    return CNN_OK;
+}
+
+int check_lrn(int N, int C, int H, int W, int size) {
+    if (N < 0 || C <= 0 || H <= 0 || W <= 0)
+        return fail(CNN_ERR_INVALID, "lrn: shape %dx%dx%dx%d", N, C, H, W);
+    if (size <= 0) return fail(CNN_ERR_INVALID, "lrn: size %d", size);
+    if (size % 2 == 0) return fail(CNN_ERR_UNSUPPORTED, "lrn: even size %d", size);
+    if (too_big(N, C, H, W)) return fail(CNN_ERR_UNSUPPORTED, "lrn: tensor exceeds 2^31-1 elements");
+    return CNN_OK;
+}
+
+int check_fc(int N, int I, int O) {
+    if (N < 0 || I <= 0 || O <= 0) return fail(CNN_ERR_INVALID, "fc: N=%d I=%d O=%d", N, I, O);
+    if (too_big(N, I) || too_big(N, O) || too_big(O, I))
+        return fail(CNN_ERR_UNSUPPORTED, "fc: tensor exceeds 2^31-1 elements");
+    return CNN_OK;
+}
+
+// ------------------------------------------------------------------ networks
+struct Plan {
+    int type;
+    int inC, inH, inW;     // input shape of the layer (per image)
+    int outC, outH, outW;  // output shape
+    int relu;              // ReLU executed inside this layer
+    bool skipped;          // a RELU layer folded into its predecessor
+    ConvShape conv;
+    PoolShape pool;
+};
+
+int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* plan,
+             int64_t* max_elems) {
+    if (!L || n <= 0) return fail(CNN_ERR_INVALID, "net: no layers");
+    if (N < 0 || C <= 0 || H <= 0 || W <= 0)
+        return fail(CNN_ERR_INVALID, "net: input %dx%dx%dx%d", N, C, H, W);
+    int c = C, h = H, w = W;
+    int64_t mx = 0;
+    int prev_exec = -1;  // index of the last executed (non-folded) layer
+    for (int i = 0; i < n; ++i) {
+        const cnn_layer_desc& d = L[i];
+        Plan& p = plan[i];
+        p = Plan{};
+        p.type = d.type;
+        p.inC = c; p.inH = h; p.inW = w;
+        int rc = CNN_OK;
+        switch (d.type) {
+            case CNN_LAYER_CONV: {
+                if (!d.weight) return fail(CNN_ERR_INVALID, "net layer %d: conv without weights", i);
+                if (d.in_channels != 0 && d.in_channels != c)
+                    return fail(CNN_ERR_INVALID, "net layer %d: conv expects %d input channels, gets %d",
+                                i, d.in_channels, c);
+                rc = check_conv(N, c, h, w, d.out_channels, d.kernel_h, d.kernel_w, d.stride_h,
+                                d.stride_w, d.pad_h, d.pad_w, d.groups, &p.conv);
+                if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
+                c = d.out_channels; h = p.conv.P; w = p.conv.Q;
+                p.relu = d.fuse_relu != 0;
+                break;
+            }
+            case CNN_LAYER_FC: {
+                if (!d.weight) return fail(CNN_ERR_INVALID, "net layer %d: fc without weights", i);
+                const int64_t I = (int64_t)c * h * w;
+                if (d.in_features != 0 && d.in_features != I)
+                    return fail(CNN_ERR_INVALID, "net layer %d: fc expects %d inputs, gets %dx%dx%d = %lld",
+                                i, d.in_features, c, h, w, (long long)I);
+                if (I > kMaxElems) return fail(CNN_ERR_UNSUPPORTED, "net layer %d: fc input too large", i);
+                rc = check_fc(N, (int)I, d.out_channels);
+                if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
+                c = d.out_channels; h = 1; w = 1;
+                p.relu = d.fuse_relu != 0;
+                break;
+            }
+            case CNN_LAYER_POOL: {
+                rc = check_pool(N, c, h, w, d.pool_mode, d.kernel_h, d.kernel_w, d.stride_h,
+                                d.stride_w, d.pad_h, d.pad_w, d.ceil_mode, &p.pool);
+                if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
+                if (d.pool_index && d.pool_mode != CNN_POOL_MAX)
+                    return fail(CNN_ERR_INVALID, "net layer %d: indices requested for average pooling", i);
+                h = p.pool.P; w = p.pool.Q;
+                p.relu = d.fuse_relu != 0;
+                break;
+            }
+            case CNN_LAYER_LRN:
+                rc = check_lrn(N, c, h, w, d.lrn_size);
+                if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
+                break;
+            case CNN_LAYER_RELU:
+                // Embedded into the preceding conv / FC / pooling layer (Sec. 3.5).
+                if (prev_exec >= 0 && (plan[prev_exec].type == CNN_LAYER_CONV ||
+                                       plan[prev_exec].type == CNN_LAYER_FC ||
+                                       plan[prev_exec].type == CNN_LAYER_POOL)) {
+                    plan[prev_exec].relu = 1;
+                    p.skipped = true;
+                }
+                break;
+            default:
+                return fail(CNN_ERR_INVALID, "net layer %d: unknown type %d", i, d.type);
+        }
+        p.outC = c; p.outH = h; p.outW = w;
+        if (too_big(N, c, h, w)) return fail(CNN_ERR_UNSUPPORTED, "net layer %d: output too large", i);
+        mx = std::max<int64_t>(mx, (int64_t)N * c * h * w);
+        if (!p.skipped) prev_exec = i;
+    }
+    *max_elems = mx;
+    return CNN_OK;
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H, int W, float* y,
+            void* ws, size_t ws_bytes, void* const* events, hipStream_t st) {
+    if (!x || !y) return fail(CNN_ERR_INVALID, "net: null input or output");
+    if (n > 4096) return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n);
+    std::vector<Plan> plan((size_t)std::max(n, 0));
+    int64_t mx = 0;
+    int rc = plan_net(L, n, N, C, H, W, plan.data(), &mx);
+    if (rc) return rc;
+    if (N == 0) {  // nothing to compute; still honour the event contract
+        for (int i = 0; events && i <= n; ++i)
+            if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), st) != hipSuccess)
+                return check_launch("hipEventRecord");
+        return CNN_OK;
+    }
+    const size_t half = align_up((size_t)mx * sizeof(float));
+    if (!ws || ws_bytes < 2 * half)
+        return fail(CNN_ERR_WORKSPACE, "net: workspace of %zu bytes, %zu needed", ws_bytes, 2 * half);
+    if (reinterpret_cast<uintptr_t>(ws) % 16)
+        return fail(CNN_ERR_INVALID, "net: workspace must be 16-byte aligned");
+    float* buf[2] = {static_cast<float*>(ws),
+                     reinterpret_cast<float*>(static_cast<char*>(ws) + half)};
+
+    int last = n - 1;
+    while (last > 0 && plan[last].skipped) --last;
+
+    const float* cur = x;
+    int next_buf = 0;
+    for (int i = 0; i < n; ++i) {
+        if (events) {
+            if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), st) != hipSuccess)
+                return check_launch("hipEventRecord");
+        }
+        const Plan& p = plan[i];
+        if (p.skipped) continue;
+        const cnn_layer_desc& d = L[i];
+        float* out = (i == last) ? y : buf[next_buf];
+        // an in-place ReLU keeps its buffer
+        if (p.type == CNN_LAYER_RELU && i != last && cur != x) out = const_cast<float*>(cur);
+        switch (p.type) {
+            case CNN_LAYER_CONV:
+                rc = launch_conv2d(p.conv, cur, d.weight, d.bias, p.relu, out, st);
+                break;
+            case CNN_LAYER_FC:
+                rc = launch_fc(cur, N, p.inC * p.inH * p.inW, d.weight, d.bias, p.outC, p.relu, out, st);
+                break;
+            case CNN_LAYER_POOL:
+                rc = launch_pool(p.pool, d.pool_mode, p.relu, cur, out, d.pool_index, st);
+                break;
+            case CNN_LAYER_LRN:
+                rc = launch_lrn(cur, N, p.inC, p.inH, p.inW, d.lrn_size, d.lrn_alpha, d.lrn_beta,
+                                d.lrn_k, out, st);
+                break;
+            case CNN_LAYER_RELU:
+                rc = launch_relu(cur, out, (int64_t)N * p.inC * p.inH * p.inW, st);
+                break;
+        }
+        if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
+        if (out == buf[next_buf]) next_buf ^= 1;
+        cur = out;
+    }
+    if (events) {
+        if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[n]), st) != hipSuccess)
+            return check_launch("hipEventRecord");
+    }
+    return CNN_OK;
+}
+
+}  // namespace
+}  // namespace cnn
+
+using namespace cnn;
+
+extern "C" {
+
+int cnn_conv2d_out_shape(int H, int W, int R, int S, int sh, int sw, int ph, int pw, int* P, int* Q) {
+    if (!P || !Q) return fail(CNN_ERR_INVALID, "conv_out_shape: null output pointer");
+    return conv_out(H, W, R, S, sh, sw, ph, pw, P, Q);
+}
+
+int cnn_pool_out_shape(int H, int W, int kh, int kw, int sh, int sw, int ph, int pw, int ceil_mode,
+                       int* P, int* Q) {
+    if (!P || !Q) return fail(CNN_ERR_INVALID, "pool_out_shape: null output pointer");
+    return pool_out(H, W, kh, kw, sh, sw, ph, pw, ceil_mode, P, Q);
+}
+
+int cnn_conv2d_fwd(const float* x, int N, int C, int H, int W, const float* w, int K, int R, int S,
+                   const float* bias, int sh, int sw, int ph, int pw, int groups, int fuse_relu,
+                   float* y, cnn_stream_t stream) {
+    if (!x || !w || !y) return fail(CNN_ERR_INVALID, "conv: null x, w or y");
+    ConvShape s;
+    int rc = check_conv(N, C, H, W, K, R, S, sh, sw, ph, pw, groups, &s);
+    if (rc) return rc;
+    return launch_conv2d(s, x, w, bias, fuse_relu != 0, y, as_stream(stream));
+}
+
+int cnn_fc_fwd(const float* x, int N, int I, const float* w, const float* bias, int O, int fuse_relu,
+               float* y, cnn_stream_t stream) {
+    if (!x || !w || !y) return fail(CNN_ERR_INVALID, "fc: null x, w or y");
+    int rc = check_fc(N, I, O);
+    if (rc) return rc;
+    return launch_fc(x, N, I, w, bias, O, fuse_relu != 0, y, as_stream(stream));
+}
+
+int cnn_pool_fwd(const float* x, int N, int C, int H, int W, int mode, int kh, int kw, int sh,
+                 int sw, int ph, int pw, int ceil_mode, int fuse_relu, float* y, int32_t* idx,
+                 cnn_stream_t stream) {
+    if (!x || !y) return fail(CNN_ERR_INVALID, "pool: null x or y");
+    PoolShape s;
+    int rc = check_pool(N, C, H, W, mode, kh, kw, sh, sw, ph, pw, ceil_mode, &s);
+    if (rc) return rc;
+    if (idx && mode != CNN_POOL_MAX) return fail(CNN_ERR_INVALID, "pool: indices need max pooling");
+    return launch_pool(s, mode, fuse_relu != 0, x, y, idx, as_stream(stream));
+}
+
+int cnn_lrn_fwd(const float* x, int N, int C, int H, int W, int size, float alpha, float beta,
+                float k, float* y, cnn_stream_t stream) {
+    if (!x || !y) return fail(CNN_ERR_INVALID, "lrn: null x or y");
+    int rc = check_lrn(N, C, H, W, size);
+    if (rc) return rc;
+    return launch_lrn(x, N, C, H, W, size, alpha, beta, k, y, as_stream(stream));
+}
+
+int cnn_relu_fwd(const float* x, float* y, int64_t n, cnn_stream_t stream) {
+    if (!x || !y) return fail(CNN_ERR_INVALID, "relu: null x or y");
+    if (n < 0) return fail(CNN_ERR_INVALID, "relu: negative length");
+    return launch_relu(x, y, n, as_stream(stream));
+}
+
+int cnn_net_out_shape(const cnn_layer_desc* layers, int n_layers, int N, int C, int H, int W,
+                      int* outC, int* outH, int* outW) {
+    if (!outC || !outH || !outW) return fail(CNN_ERR_INVALID, "net_out_shape: null output pointer");
+    if (n_layers > 4096) return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n_layers);
+    std::vector<Plan> plan((size_t)std::max(n_layers, 0));
+    int64_t mx;
+    int rc = plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx);
+    if (rc) return rc;
+    *outC = plan[n_layers - 1].outC;
+    *outH = plan[n_layers - 1].outH;
+    *outW = plan[n_layers - 1].outW;
+    return CNN_OK;
+}
+
+size_t cnn_net_workspace_bytes(const cnn_layer_desc* layers, int n_layers, int N, int C, int H, int W) {
+    if (n_layers > 4096 || n_layers <= 0) return 0;
+    std::vector<Plan> plan((size_t)n_layers);
+    int64_t mx;
+    if (plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx)) return 0;
+    return 2 * align_up((size_t)mx * sizeof(float));
+}
+
+int cnn_net_fwd(const cnn_layer_desc* layers, int n_layers, const float* x, int N, int C, int H,
+                int W, float* y, void* ws, size_t ws_bytes, cnn_stream_t stream) {
+    return run_net(layers, n_layers, x, N, C, H, W, y, ws, ws_bytes, nullptr, as_stream(stream));
+}
+
+int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x, int N, int C,
+                      int H, int W, float* y, void* ws, size_t ws_bytes, void* const* events,
+                      cnn_stream_t stream) {
+    if (!events) return fail(CNN_ERR_INVALID, "net_fwd_timed: null events");
+    return run_net(layers, n_layers, x, N, C, H, W, y, ws, ws_bytes, events, as_stream(stream));
+}
+
+const char* cnn_last_error(void) { return g_err; }
+
+const char* cnn_version(void) { return "libcnn 0.1 gfx950"; }
+
+}  // extern "C"

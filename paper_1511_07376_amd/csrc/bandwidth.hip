@@ -1,0 +1,226 @@
+// Pooling, local response normalization and ReLU: layers that move far more
+// bytes than they compute, so each kernel reads its input once from HBM with
+// consecutive lanes on consecutive addresses and writes its output once.
+#include "common.h"
+
+#include <algorithm>
+
+namespace cnn {
+namespace {
+
+constexpr int kThreads = 256;
+
+inline int grid_for(int64_t items, int per_thread = 1) {
+    const int64_t blocks = (items + (int64_t)kThreads * per_thread - 1) / ((int64_t)kThreads * per_thread);
+    return (int)std::max<int64_t>(1, std::min<int64_t>(blocks, 1 << 20));
+}
+
+// ------------------------------------------------------------------ pooling
+// One thread per output element, lanes along the output row, so the lanes of
+// a wave read neighbouring windows of the same input rows.
+struct PoolParams {
+    const float* x;
+    float* y;
+    int32_t* idx;
+    int H, W, P, Q, kh, kw, sh, sw, ph, pw;
+    int total;  // N*C*P*Q
+    int relu;
+};
+
+template <bool WITH_IDX>
+__global__ void __launch_bounds__(kThreads) maxpool_f32(PoolParams p) {
+    for (int o = blockIdx.x * kThreads + threadIdx.x; o < p.total; o += gridDim.x * kThreads) {
+        const int q = o % p.Q;
+        const int t = o / p.Q;
+        const int pp = t % p.P;
+        const int nc = t / p.P;
+        const float* plane = p.x + nc * p.H * p.W;
+        const int hs = pp * p.sh - p.ph, ws = q * p.sw - p.pw;
+        const int h0 = max(hs, 0), w0 = max(ws, 0);
+        const int h1 = min(hs + p.kh, p.H), w1 = min(ws + p.kw, p.W);
+        // first maximum in row-major order: strict comparison
+        int bi = h0 * p.W + w0;
+        float best = plane[bi];
+        for (int h = h0; h < h1; ++h) {
+            const float* row = plane + h * p.W;
+            for (int w = w0; w < w1; ++w) {
+                const float v = row[w];
+                if (v > best) {
+                    best = v;
+                    bi = h * p.W + w;
+                }
+            }
+        }
+        if (p.relu) best = best > 0.0f ? best : 0.0f;
+        p.y[o] = best;
+        if (WITH_IDX) p.idx[o] = bi;
+    }
+}
+
+__global__ void __launch_bounds__(kThreads) avgpool_f32(PoolParams p) {
+    for (int o = blockIdx.x * kThreads + threadIdx.x; o < p.total; o += gridDim.x * kThreads) {
+        const int q = o % p.Q;
+        const int t = o / p.Q;
+        const int pp = t % p.P;
+        const int nc = t / p.P;
+        const float* plane = p.x + nc * p.H * p.W;
+        const int hs = pp * p.sh - p.ph, ws = q * p.sw - p.pw;
+        // divisor: the window clipped to the padded extent
+        const int count = (min(hs + p.kh, p.H + p.ph) - hs) * (min(ws + p.kw, p.W + p.pw) - ws);
+        const int h0 = max(hs, 0), w0 = max(ws, 0);
+        const int h1 = min(hs + p.kh, p.H), w1 = min(ws + p.kw, p.W);
+        float sum = 0.0f;
+        for (int h = h0; h < h1; ++h) {
+            const float* row = plane + h * p.W;
+            for (int w = w0; w < w1; ++w) sum += row[w];
+        }
+        float v = sum / (float)count;
+        if (p.relu) v = v > 0.0f ? v : 0.0f;
+        p.y[o] = v;
+    }
+}
+
+// ------------------------------------------------------------------ LRN
+// One thread per pixel column (n, h, w); it walks the channels keeping the
+// HALF values on each side of the current channel in registers, so every
+// input element is read from memory once.  Lanes cover consecutive w.
+struct LrnParams {
+    const float* x;
+    float* y;
+    int C, HW;
+    int total;  // N*H*W
+    float alpha_over_size, beta, k;
+};
+
+template <int HALF>
+__global__ void __launch_bounds__(kThreads) lrn_across_f32(LrnParams p) {
+    constexpr int WIN = 2 * HALF + 1;
+    for (int t = blockIdx.x * kThreads + threadIdx.x; t < p.total; t += gridDim.x * kThreads) {
+        const int n = t / p.HW;
+        const int hw = t - n * p.HW;
+        const float* xp = p.x + n * p.C * p.HW + hw;
+        float* yp = p.y + n * p.C * p.HW + hw;
+        // win[j] holds channel c - HALF + j (0 outside [0, C))
+        float win[WIN];
+#pragma unroll
+        for (int j = 0; j < WIN; ++j) {
+            const int cc = j - HALF;
+            win[j] = (cc >= 0 && cc < p.C) ? xp[cc * p.HW] : 0.0f;
+        }
+        for (int c = 0; c < p.C; ++c) {
+            float sq = 0.0f;
+#pragma unroll
+            for (int j = 0; j < WIN; ++j) sq += win[j] * win[j];
+            const float scale = p.k + p.alpha_over_size * sq;
+            yp[c * p.HW] = win[HALF] * powf(scale, -p.beta);
+#pragma unroll
+            for (int j = 0; j < WIN - 1; ++j) win[j] = win[j + 1];
+            const int cn = c + HALF + 1;
+            win[WIN - 1] = cn < p.C ? xp[cn * p.HW] : 0.0f;
+        }
+    }
+}
+
+// Any odd size: recompute the clipped window sum for every channel.
+__global__ void __launch_bounds__(kThreads) lrn_across_any_f32(LrnParams p, int half) {
+    for (int t = blockIdx.x * kThreads + threadIdx.x; t < p.total; t += gridDim.x * kThreads) {
+        const int n = t / p.HW;
+        const int hw = t - n * p.HW;
+        const float* xp = p.x + n * p.C * p.HW + hw;
+        float* yp = p.y + n * p.C * p.HW + hw;
+        for (int c = 0; c < p.C; ++c) {
+            const int c0 = max(c - half, 0), c1 = min(c + half, p.C - 1);
+            float sq = 0.0f;
+            for (int cc = c0; cc <= c1; ++cc) {
+                const float v = xp[cc * p.HW];
+                sq += v * v;
+            }
+            const float scale = p.k + p.alpha_over_size * sq;
+            yp[c * p.HW] = xp[c * p.HW] * powf(scale, -p.beta);
+        }
+    }
+}
+
+// ------------------------------------------------------------------ ReLU
+__device__ inline float relu1(float v) { return v > 0.0f ? v : 0.0f; }
+
+__global__ void __launch_bounds__(kThreads) relu_f32x4(const float4* x, float4* y, int64_t n4) {
+    for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < n4;
+         i += (int64_t)gridDim.x * kThreads) {
+        const float4 v = x[i];
+        y[i] = make_float4(relu1(v.x), relu1(v.y), relu1(v.z), relu1(v.w));
+    }
+}
+
+__global__ void __launch_bounds__(kThreads) relu_f32(const float* x, float* y, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * kThreads)
+        y[i] = relu1(x[i]);
+}
+
+}  // namespace
+
+int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y, int32_t* idx,
+                hipStream_t st) {
+    PoolParams p;
+    p.x = x;
+    p.y = y;
+    p.idx = idx;
+    p.H = s.H; p.W = s.W; p.P = s.P; p.Q = s.Q;
+    p.kh = s.kh; p.kw = s.kw; p.sh = s.sh; p.sw = s.sw; p.ph = s.ph; p.pw = s.pw;
+    p.total = s.N * s.C * s.P * s.Q;
+    p.relu = relu;
+    if (p.total == 0) return CNN_OK;
+    const dim3 grid(grid_for(p.total)), block(kThreads);
+    if (mode == CNN_POOL_MAX) {
+        if (idx)
+            hipLaunchKernelGGL(maxpool_f32<true>, grid, block, 0, st, p);
+        else
+            hipLaunchKernelGGL(maxpool_f32<false>, grid, block, 0, st, p);
+        return check_launch("maxpool_f32");
+    }
+    hipLaunchKernelGGL(avgpool_f32, grid, block, 0, st, p);
+    return check_launch("avgpool_f32");
+}
+
+int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha, float beta,
+               float k, float* y, hipStream_t st) {
+    LrnParams p;
+    p.x = x;
+    p.y = y;
+    p.C = C;
+    p.HW = H * W;
+    p.total = N * H * W;
+    p.alpha_over_size = alpha / (float)size;
+    p.beta = beta;
+    p.k = k;
+    if (p.total == 0) return CNN_OK;
+    const dim3 grid(grid_for(p.total)), block(kThreads);
+    switch (size / 2) {
+        case 0: hipLaunchKernelGGL(lrn_across_f32<0>, grid, block, 0, st, p); break;
+        case 1: hipLaunchKernelGGL(lrn_across_f32<1>, grid, block, 0, st, p); break;
+        case 2: hipLaunchKernelGGL(lrn_across_f32<2>, grid, block, 0, st, p); break;
+        case 3: hipLaunchKernelGGL(lrn_across_f32<3>, grid, block, 0, st, p); break;
+        case 4: hipLaunchKernelGGL(lrn_across_f32<4>, grid, block, 0, st, p); break;
+        default: hipLaunchKernelGGL(lrn_across_any_f32, grid, block, 0, st, p, size / 2); break;
+    }
+    return check_launch("lrn_across_f32");
+}
+
+int launch_relu(const float* x, float* y, int64_t n, hipStream_t st) {
+    if (n == 0) return CNN_OK;
+    const bool vec = ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(y)) & 15) == 0;
+    int64_t done = 0;
+    if (vec && n >= 4) {
+        const int64_t n4 = n / 4;
+        hipLaunchKernelGGL(relu_f32x4, dim3(grid_for(n4, 4)), dim3(kThreads), 0, st,
+                           reinterpret_cast<const float4*>(x), reinterpret_cast<float4*>(y), n4);
+        done = n4 * 4;
+    }
+    if (done < n)
+        hipLaunchKernelGGL(relu_f32, dim3(grid_for(n - done)), dim3(kThreads), 0, st, x + done,
+                           y + done, n - done);
+    return check_launch("relu_f32");
+}
+
+}  // namespace cnn

@@ -1,0 +1,50 @@
+// Internal declarations shared by the libcnn translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "../../include/cnn.h"
+
+namespace cnn {
+
+// Records a thread-local error message and returns `status`.
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+// Checks hipGetLastError() after launches; CNN_OK or CNN_ERR_HIP.
+int check_launch(const char* what);
+
+inline hipStream_t as_stream(cnn_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
+
+inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Largest element count a tensor may have (offsets inside kernels are int32).
+constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
+
+struct ConvShape {
+    int N, C, H, W, K, R, S, sh, sw, ph, pw, G, P, Q;
+};
+
+struct PoolShape {
+    int N, C, H, W, kh, kw, sh, sw, ph, pw, P, Q;
+};
+
+// Shape helpers (return CNN_OK or an error status with a message).
+int conv_out(int H, int W, int R, int S, int sh, int sw, int ph, int pw, int* P, int* Q);
+int pool_out(int H, int W, int kh, int kw, int sh, int sw, int ph, int pw, int ceil_mode,
+             int* P, int* Q);
+
+// Launchers: arguments already validated; they enqueue and return CNN_OK or
+// CNN_ERR_HIP.
+int launch_conv2d(const ConvShape& s, const float* x, const float* w, const float* bias,
+                  int relu, float* y, hipStream_t st);
+int launch_fc(const float* x, int N, int I, const float* w, const float* bias, int O, int relu,
+              float* y, hipStream_t st);
+int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y, int32_t* idx,
+                hipStream_t st);
+int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha, float beta,
+               float k, float* y, hipStream_t st);
+int launch_relu(const float* x, float* y, int64_t n, hipStream_t st);
+
+}  // namespace cnn

@@ -1,0 +1,175 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/cnn.h declares, its host-side shape helpers agree with the oracle's,
+and invalid arguments are rejected before any launch.
+
+No call here enqueues GPU work: every compute entry point is called only
+with arguments that its host-side validation rejects.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+from paper_1511_07376_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cnn.h")
+
+cnn = pytest.importorskip("paper_1511_07376_amd.cnn", reason="libcnn.so not built")
+
+FAKE = 0x1000  # a non-null pointer that is never dereferenced (validation fails first)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*[A-Za-z_][\w\s\*]*?\b(cnn_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert len(names) >= 13, names
+    for name in names:
+        assert hasattr(cnn.lib, name), f"{name} declared in cnn.h but not exported"
+    assert set(names) == set(cnn.EXPORTED)
+
+
+def test_version_and_empty_error():
+    assert "gfx950" in cnn.cnn_version()
+
+
+def test_layer_desc_layout_matches_header():
+    # 13 int32 + 3 float + 2 int32 = 72 bytes, then three pointers
+    assert ctypes.sizeof(cnn.cnn_layer_desc) == 96
+    assert cnn.cnn_layer_desc.weight.offset == 72
+
+
+@pytest.mark.parametrize("H,R,s,p", [(227, 11, 4, 0), (27, 5, 1, 2), (13, 3, 1, 1), (28, 5, 1, 0),
+                                     (224, 7, 2, 3), (56, 1, 1, 0), (9, 4, 3, 2), (5, 5, 1, 0)])
+def test_conv_out_shape_agrees_with_oracle(H, R, s, p):
+    assert cnn.cnn_conv2d_out_shape(H, H + 3, R, R, s, p) == \
+        oracle.conv2d_out_shape(H, H + 3, R, R, s, s, p, p)
+
+
+def test_pool_out_shape_agrees_with_oracle_exhaustive():
+    for H in range(1, 20):
+        for k in range(1, 5):
+            for s in range(1, 5):
+                for p in range(0, k):
+                    for ceil in (True, False):
+                        if H + 2 * p < k:
+                            continue
+                        assert cnn.cnn_pool_out_shape(H, H, k, s, p, ceil) == \
+                            oracle.pool_out_shape(H, H, k, k, s, s, p, p, ceil), (H, k, s, p, ceil)
+
+
+@pytest.mark.parametrize("name,out", [("lenet", (16, 10)), ("cifar_quick", (32, 10)),
+                                      ("alexnet", (64, 1000))])
+def test_net_out_shape_and_workspace(name, out):
+    net = wl.NETS[name]
+    descs = _descs(net)
+    C, H, W = net.input_chw
+    oc, oh, ow = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    rc = cnn.lib.cnn_net_out_shape(descs, len(descs), out[0], C, H, W, ctypes.byref(oc),
+                                   ctypes.byref(oh), ctypes.byref(ow))
+    assert rc == 0, cnn.cnn_last_error()
+    assert (oc.value, oh.value, ow.value) == (out[1], 1, 1)
+    ws = cnn.lib.cnn_net_workspace_bytes(descs, len(descs), out[0], C, H, W)
+    # two 256-byte aligned buffers of the largest activation
+    biggest = max(a.size for a in oracle.net_fwd(net, wl.make_input(net, 1), wl.make_params(net),
+                                                 keep=True)[1]) * out[0] * 4
+    half = (biggest + 255) // 256 * 256
+    assert ws == 2 * half
+
+
+def _descs(net):
+    """Descriptors with fake (never dereferenced) weight pointers."""
+    descs = (cnn.cnn_layer_desc * len(net.layers))()
+    for i, layer in enumerate(net.layers):
+        d = descs[i]
+        if layer.kind == "conv":
+            d.type, d.out_channels = cnn.CNN_LAYER_CONV, layer.out_channels
+            d.in_channels = layer.in_channels
+            d.kernel_h, d.kernel_w = layer.kernel
+            d.stride_h, d.stride_w = layer.stride
+            d.pad_h, d.pad_w = layer.pad
+            d.groups, d.fuse_relu, d.weight = layer.groups, int(layer.relu), FAKE
+        elif layer.kind == "fc":
+            d.type, d.out_channels, d.in_features = cnn.CNN_LAYER_FC, layer.out_features, layer.in_features
+            d.fuse_relu, d.weight = int(layer.relu), FAKE
+        elif layer.kind == "pool":
+            d.type = cnn.CNN_LAYER_POOL
+            d.pool_mode = 0 if layer.mode == "max" else 1
+            d.kernel_h, d.kernel_w = layer.kernel
+            d.stride_h, d.stride_w = layer.stride
+            d.pad_h, d.pad_w = layer.pad
+            d.ceil_mode, d.fuse_relu = int(layer.ceil), int(layer.relu)
+        elif layer.kind == "lrn":
+            d.type, d.lrn_size = cnn.CNN_LAYER_LRN, layer.size
+            d.lrn_alpha, d.lrn_beta, d.lrn_k = layer.alpha, layer.beta, layer.k
+        else:
+            d.type = cnn.CNN_LAYER_RELU
+    return descs
+
+
+# ---------------------------------------------------------------- rejected arguments
+L = cnn.lib
+
+
+@pytest.mark.parametrize("args,status", [
+    # (x, N, C, H, W, w, K, R, S, bias, sh, sw, ph, pw, G, relu, y, stream)
+    ((0, 1, 3, 8, 8, FAKE, 4, 3, 3, 0, 1, 1, 0, 0, 1, 0, FAKE, 0), cnn.CNN_ERR_INVALID),       # null x
+    ((FAKE, 1, 3, 8, 8, FAKE, 4, 3, 3, 0, 1, 1, 0, 0, 1, 0, 0, 0), cnn.CNN_ERR_INVALID),       # null y
+    ((FAKE, 1, 3, 8, 8, FAKE, 4, 3, 3, 0, 0, 1, 0, 0, 1, 0, FAKE, 0), cnn.CNN_ERR_INVALID),    # stride 0
+    ((FAKE, 1, 3, 8, 8, FAKE, 4, 3, 3, 0, 1, 1, 0, 0, 2, 0, FAKE, 0), cnn.CNN_ERR_INVALID),    # 2 !| 3
+    ((FAKE, 1, 4, 8, 8, FAKE, 6, 3, 3, 0, 1, 1, 0, 0, 4, 0, FAKE, 0), cnn.CNN_ERR_INVALID),    # 4 !| 6
+    ((FAKE, 1, 3, 2, 2, FAKE, 4, 3, 3, 0, 1, 1, 0, 0, 1, 0, FAKE, 0), cnn.CNN_ERR_INVALID),    # kernel > input
+    ((FAKE, -1, 3, 8, 8, FAKE, 4, 3, 3, 0, 1, 1, 0, 0, 1, 0, FAKE, 0), cnn.CNN_ERR_INVALID),   # N < 0
+    ((FAKE, 1, 3, 8, 8, FAKE, 4, 3, 3, 0, 1, 1, -1, 0, 1, 0, FAKE, 0), cnn.CNN_ERR_INVALID),   # pad < 0
+    ((FAKE, 70000, 64, 224, 224, FAKE, 4, 3, 3, 0, 1, 1, 1, 1, 1, 0, FAKE, 0), cnn.CNN_ERR_UNSUPPORTED),
+])
+def test_conv_rejects(args, status):
+    assert L.cnn_conv2d_fwd(*args) == status
+    assert cnn.cnn_last_error().startswith("conv")
+
+
+def test_fc_pool_lrn_relu_reject():
+    assert L.cnn_fc_fwd(FAKE, 4, 0, FAKE, 0, 10, 0, FAKE, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_fc_fwd(0, 4, 8, FAKE, 0, 10, 0, FAKE, 0) == cnn.CNN_ERR_INVALID
+    # pool: pad must be below the window; indices need max mode; bad mode
+    assert L.cnn_pool_fwd(FAKE, 1, 1, 8, 8, 0, 2, 2, 2, 2, 2, 0, 1, 0, FAKE, 0, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_pool_fwd(FAKE, 1, 1, 8, 8, 1, 2, 2, 2, 2, 0, 0, 1, 0, FAKE, FAKE, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_pool_fwd(FAKE, 1, 1, 8, 8, 7, 2, 2, 2, 2, 0, 0, 1, 0, FAKE, 0, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_lrn_fwd(FAKE, 1, 4, 4, 4, 4, 1e-4, 0.75, 1.0, FAKE, 0) == cnn.CNN_ERR_UNSUPPORTED
+    assert L.cnn_lrn_fwd(FAKE, 1, 4, 4, 4, 0, 1e-4, 0.75, 1.0, FAKE, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_relu_fwd(FAKE, FAKE, -1, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_relu_fwd(0, FAKE, 4, 0) == cnn.CNN_ERR_INVALID
+
+
+def test_net_rejects_before_launch():
+    net = wl.alexnet
+    C, H, W = net.input_chw
+    descs = _descs(net)
+    n = len(descs)
+    # workspace too small
+    assert L.cnn_net_fwd(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1024, 0) == cnn.CNN_ERR_WORKSPACE
+    assert "workspace" in cnn.cnn_last_error()
+    # FC input size inconsistent with the layer chain
+    descs[10].in_features = 9000
+    assert L.cnn_net_fwd(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, 0) == cnn.CNN_ERR_INVALID
+    assert "layer 10" in cnn.cnn_last_error()
+    descs[10].in_features = 9216
+    # missing weights
+    descs[0].weight = None
+    assert L.cnn_net_fwd(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, 0) == cnn.CNN_ERR_INVALID
+    descs[0].weight = FAKE
+    # unknown layer type, no layers, input channels different from the first conv's
+    descs[1].type = 9
+    assert L.cnn_net_fwd(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, 0) == cnn.CNN_ERR_INVALID
+    descs[1].type = cnn.CNN_LAYER_LRN
+    assert L.cnn_net_fwd(descs, 0, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_net_fwd(descs, n, FAKE, 2, 4, H, W, FAKE, FAKE, 1 << 40, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_net_fwd_timed(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, None, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_net_workspace_bytes(descs, 0, 2, C, H, W) == 0

