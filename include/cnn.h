@@ -16,7 +16,8 @@
  *    enqueued on `stream` (a hipStream_t; NULL = the null stream) and the
  *    caller synchronises.
  *  - Input and output buffers must not overlap, except that cnn_relu_fwd
- *    allows y == x.
+ *    allows y == x.  A pointer to a tensor with no elements (batch N = 0,
+ *    length n = 0) may be NULL; such a call validates and enqueues nothing.
  *  - No exception or abort crosses the ABI.  cnn_last_error() returns a
  *    thread-local message describing the last non-OK status of this thread.
  *  - Sizes are int (each tensor must hold fewer than 2^31 elements).

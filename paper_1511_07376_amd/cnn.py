@@ -264,7 +264,8 @@ class Network:
         oc, oh, ow = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
         _ok(lib.cnn_net_out_shape(self.descs, len(self.descs), N, C, H, W, ctypes.byref(oc),
                                   ctypes.byref(oh), ctypes.byref(ow)))
-        if self.net.layers[-1].kind == "fc":
+        last = [l for l in self.net.layers if l.kind != "relu"]
+        if last and last[-1].kind == "fc":
             return (N, oc.value)
         return (N, oc.value, oh.value, ow.value)
 

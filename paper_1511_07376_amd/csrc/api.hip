@@ -215,7 +215,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H, int W, float* y,
             void* ws, size_t ws_bytes, void* const* events, hipStream_t st) {
-    if (!x || !y) return fail(CNN_ERR_INVALID, "net: null input or output");
+    if (N != 0 && (!x || !y)) return fail(CNN_ERR_INVALID, "net: null input or output");
     if (n > 4096) return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n);
     std::vector<Plan> plan((size_t)std::max(n, 0));
     int64_t mx = 0;
@@ -301,7 +301,7 @@ int cnn_pool_out_shape(int H, int W, int kh, int kw, int sh, int sw, int ph, int
 int cnn_conv2d_fwd(const float* x, int N, int C, int H, int W, const float* w, int K, int R, int S,
                    const float* bias, int sh, int sw, int ph, int pw, int groups, int fuse_relu,
                    float* y, cnn_stream_t stream) {
-    if (!x || !w || !y) return fail(CNN_ERR_INVALID, "conv: null x, w or y");
+    if ((N != 0 && (!x || !y)) || !w) return fail(CNN_ERR_INVALID, "conv: null x, w or y");
     ConvShape s;
     int rc = check_conv(N, C, H, W, K, R, S, sh, sw, ph, pw, groups, &s);
     if (rc) return rc;
@@ -310,7 +310,7 @@ int cnn_conv2d_fwd(const float* x, int N, int C, int H, int W, const float* w, i
 
 int cnn_fc_fwd(const float* x, int N, int I, const float* w, const float* bias, int O, int fuse_relu,
                float* y, cnn_stream_t stream) {
-    if (!x || !w || !y) return fail(CNN_ERR_INVALID, "fc: null x, w or y");
+    if ((N != 0 && (!x || !y)) || !w) return fail(CNN_ERR_INVALID, "fc: null x, w or y");
     int rc = check_fc(N, I, O);
     if (rc) return rc;
     return launch_fc(x, N, I, w, bias, O, fuse_relu != 0, y, as_stream(stream));
@@ -319,7 +319,7 @@ int cnn_fc_fwd(const float* x, int N, int I, const float* w, const float* bias, 
 int cnn_pool_fwd(const float* x, int N, int C, int H, int W, int mode, int kh, int kw, int sh,
                  int sw, int ph, int pw, int ceil_mode, int fuse_relu, float* y, int32_t* idx,
                  cnn_stream_t stream) {
-    if (!x || !y) return fail(CNN_ERR_INVALID, "pool: null x or y");
+    if (N != 0 && (!x || !y)) return fail(CNN_ERR_INVALID, "pool: null x or y");
     PoolShape s;
     int rc = check_pool(N, C, H, W, mode, kh, kw, sh, sw, ph, pw, ceil_mode, &s);
     if (rc) return rc;
@@ -329,14 +329,14 @@ int cnn_pool_fwd(const float* x, int N, int C, int H, int W, int mode, int kh, i
 
 int cnn_lrn_fwd(const float* x, int N, int C, int H, int W, int size, float alpha, float beta,
                 float k, float* y, cnn_stream_t stream) {
-    if (!x || !y) return fail(CNN_ERR_INVALID, "lrn: null x or y");
+    if (N != 0 && (!x || !y)) return fail(CNN_ERR_INVALID, "lrn: null x or y");
     int rc = check_lrn(N, C, H, W, size);
     if (rc) return rc;
     return launch_lrn(x, N, C, H, W, size, alpha, beta, k, y, as_stream(stream));
 }
 
 int cnn_relu_fwd(const float* x, float* y, int64_t n, cnn_stream_t stream) {
-    if (!x || !y) return fail(CNN_ERR_INVALID, "relu: null x or y");
+    if (n != 0 && (!x || !y)) return fail(CNN_ERR_INVALID, "relu: null x or y");
     if (n < 0) return fail(CNN_ERR_INVALID, "relu: negative length");
     return launch_relu(x, y, n, as_stream(stream));
 }
