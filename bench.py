@@ -120,6 +120,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for the CPU baseline (0 disables it)")
+    ap.add_argument("--no-autotune", dest="autotune", action="store_false",
+                    help="use the built-in tile heuristic instead of tuning during warm-up")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
@@ -140,8 +142,14 @@ def main():
     yd = torch.empty(model.out_shape(batch), device="cuda")
 
     nl = len(net.layers)
-    for _ in range(args.warmup):
+    # The auto-tuner (the paper's first-launch tuning, Sec. 3.6) picks each conv
+    # layer's tile configuration during the first warm-up step; the timed steps
+    # use the recorded choices.
+    if args.autotune:
+        cnn.cnn_set_autotune(True)
+    for _ in range(max(args.warmup, 1 if args.autotune else 0)):
         model(xd, y=yd)
+    cnn.cnn_set_autotune(False)
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(nl + 1)] for _ in range(args.steps)]
     for evs in events:
         for e in evs:
@@ -210,6 +218,9 @@ def main():
         "conv_gflops": round(conv_tf * 1e3, 1),
         "conv_frac_fp32_mfma_peak": round(conv_tf / PEAK_FP32_MFMA_TFLOPS, 4),
         "conv_ms": round(conv_ms, 5),
+        "autotune": bool(args.autotune),
+        "conv_configs": {" ".join(l.split()[:-1]): cnn.cnn_conv2d_config_name(int(l.split()[-1]))
+                         for l in cnn.cnn_tuning_export().splitlines()},
         "layers": layers,
         "roofline": roof,
     }

@@ -70,6 +70,48 @@ int cnn_conv2d_fwd(const float* x, int N, int C, int H, int W,
                    int sh, int sw, int ph, int pw, int groups, int fuse_relu,
                    float* y, cnn_stream_t stream);
 
+/* ---------------------------------------------------------------- tuning
+ * The paper's library has tuning parameters that set the work per GPU thread
+ * and per SIMD unit, and an optional auto-tuner that times predefined
+ * scenarios on first launch and keeps the fastest (Sec. 3.6).  Here the
+ * tuning parameter is the convolution kernel's tile configuration.
+ */
+
+/* Number of convolution tile configurations in this build, and a readable
+ * name for configuration i (NULL when out of range). */
+int cnn_conv2d_num_configs(void);
+const char* cnn_conv2d_config_name(int i);
+
+/* cnn_conv2d_fwd with an explicit tile configuration: 0 <= config <
+ * cnn_conv2d_num_configs(), or -1 for the built-in heuristic (ignoring any
+ * tuned entry).  Every configuration computes the same function. */
+int cnn_conv2d_fwd_config(const float* x, int N, int C, int H, int W,
+                          const float* w, int K, int R, int S, const float* bias,
+                          int sh, int sw, int ph, int pw, int groups, int fuse_relu,
+                          float* y, int config, cnn_stream_t stream);
+
+/* Auto-tuning switch (process-wide; default 0 = off).  With 1, the first
+ * cnn_conv2d_fwd / cnn_net_fwd call that meets a new convolution shape runs
+ * every configuration on that call's own buffers, synchronising its stream
+ * (not while the stream is being captured), and records the fastest for the
+ * shape; the call then returns normally with the result of the chosen
+ * configuration.  Later calls of the shape use the record, tuning on or off. */
+int cnn_set_autotune(int mode);
+
+/* The tuning records as text, one line per shape:
+ *   "N C H W K R S sh sw ph pw G config\n".
+ * Writes at most cap bytes (NUL-terminated) to buf when buf is not NULL and
+ * returns the size the whole text needs, NUL included. */
+size_t cnn_tuning_export(char* buf, size_t cap);
+
+/* Adds records in the export format (lines starting with '#' are skipped);
+ * returns the number of records read, or CNN_ERR_INVALID on a malformed line
+ * (records before it are kept). */
+int cnn_tuning_import(const char* text);
+
+/* Forgets every tuning record. */
+int cnn_tuning_clear(void);
+
 /* Fully-connected layer (Sec. 3.1; a matrix-vector product per image,
  * Sec. 3.5): y[n,o] = b[o] + sum_i x[n,i] * w[o,i].
  *   x [N][I] (an NCHW tensor flattened: i = c*H*W + h*W + w)

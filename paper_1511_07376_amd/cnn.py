@@ -63,17 +63,29 @@ lib.cnn_net_workspace_bytes.restype = ctypes.c_size_t
 lib.cnn_net_fwd.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t, _p]
 lib.cnn_net_fwd_timed.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
                                   ctypes.POINTER(ctypes.c_void_p), _p]
+lib.cnn_conv2d_fwd_config.argtypes = lib.cnn_conv2d_fwd.argtypes[:17] + [_i, _p]
+lib.cnn_conv2d_num_configs.argtypes = []
+lib.cnn_conv2d_config_name.argtypes = [_i]
+lib.cnn_conv2d_config_name.restype = ctypes.c_char_p
+lib.cnn_set_autotune.argtypes = [_i]
+lib.cnn_tuning_export.argtypes = [ctypes.c_char_p, ctypes.c_size_t]
+lib.cnn_tuning_export.restype = ctypes.c_size_t
+lib.cnn_tuning_import.argtypes = [ctypes.c_char_p]
+lib.cnn_tuning_clear.argtypes = []
 lib.cnn_last_error.restype = ctypes.c_char_p
 lib.cnn_version.restype = ctypes.c_char_p
 for _name in ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
               "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_net_out_shape", "cnn_net_fwd",
-              "cnn_net_fwd_timed"):
+              "cnn_net_fwd_timed", "cnn_conv2d_fwd_config", "cnn_conv2d_num_configs",
+              "cnn_set_autotune", "cnn_tuning_import", "cnn_tuning_clear"):
     getattr(lib, _name).restype = _i
 
 EXPORTED = ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
             "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_net_out_shape",
             "cnn_net_workspace_bytes", "cnn_net_fwd", "cnn_net_fwd_timed", "cnn_last_error",
-            "cnn_version")
+            "cnn_version", "cnn_conv2d_num_configs", "cnn_conv2d_config_name",
+            "cnn_conv2d_fwd_config", "cnn_set_autotune", "cnn_tuning_export",
+            "cnn_tuning_import", "cnn_tuning_clear")
 
 
 class CnnError(RuntimeError):
@@ -137,8 +149,12 @@ def cnn_pool_out_shape(H, W, kernel, stride, pad=0, ceil_mode=True) -> Tuple[int
     return P.value, Q.value
 
 
-def cnn_conv2d_fwd(x, w, bias=None, stride=1, pad=0, groups=1, fuse_relu=False, y=None, stream=None):
-    """x [N][C][H][W], w [K][C/G][R][S], bias [K] -> y [N][K][P][Q] (allocated if None)."""
+def cnn_conv2d_fwd(x, w, bias=None, stride=1, pad=0, groups=1, fuse_relu=False, y=None, stream=None,
+                   config=None):
+    """x [N][C][H][W], w [K][C/G][R][S], bias [K] -> y [N][K][P][Q] (allocated if None).
+
+    config=None uses the tuned / heuristic tile configuration (cnn_conv2d_fwd);
+    an int calls cnn_conv2d_fwd_config with that configuration (-1: heuristic)."""
     N, C, H, W = x.shape
     K, _cg, R, S = w.shape
     sh, sw = _pair(stride)
@@ -146,9 +162,44 @@ def cnn_conv2d_fwd(x, w, bias=None, stride=1, pad=0, groups=1, fuse_relu=False, 
     if y is None:
         P, Q = cnn_conv2d_out_shape(H, W, R, S, (sh, sw), (ph, pw))
         y = torch.empty((N, K, P, Q), dtype=torch.float32, device=x.device)
-    _ok(lib.cnn_conv2d_fwd(_dev(x, "x"), N, C, H, W, _dev(w, "w"), K, R, S, _dev(bias, "bias"),
-                           sh, sw, ph, pw, groups, int(fuse_relu), _dev(y, "y"), _stream(stream)))
+    args = (_dev(x, "x"), N, C, H, W, _dev(w, "w"), K, R, S, _dev(bias, "bias"),
+            sh, sw, ph, pw, groups, int(fuse_relu), _dev(y, "y"))
+    if config is None:
+        _ok(lib.cnn_conv2d_fwd(*args, _stream(stream)))
+    else:
+        _ok(lib.cnn_conv2d_fwd_config(*args, int(config), _stream(stream)))
     return y
+
+
+def cnn_conv2d_num_configs() -> int:
+    return int(lib.cnn_conv2d_num_configs())
+
+
+def cnn_conv2d_config_name(i: int) -> Optional[str]:
+    r = lib.cnn_conv2d_config_name(int(i))
+    return None if r is None else r.decode()
+
+
+def cnn_set_autotune(on: bool) -> None:
+    _ok(lib.cnn_set_autotune(int(bool(on))))
+
+
+def cnn_tuning_export() -> str:
+    n = lib.cnn_tuning_export(None, 0)
+    buf = ctypes.create_string_buffer(n)
+    lib.cnn_tuning_export(buf, n)
+    return buf.value.decode()
+
+
+def cnn_tuning_import(text: str) -> int:
+    rc = lib.cnn_tuning_import(text.encode())
+    if rc < 0:
+        raise CnnError(rc, cnn_last_error())
+    return rc
+
+
+def cnn_tuning_clear() -> None:
+    _ok(lib.cnn_tuning_clear())
 
 
 def cnn_fc_fwd(x, w, bias=None, fuse_relu=False, y=None, stream=None):

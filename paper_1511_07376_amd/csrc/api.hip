@@ -253,7 +253,7 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
         if (p.type == CNN_LAYER_RELU && i != last && cur != x) out = const_cast<float*>(cur);
         switch (p.type) {
             case CNN_LAYER_CONV:
-                rc = launch_conv2d(p.conv, cur, d.weight, d.bias, p.relu, out, st);
+                rc = conv2d_dispatch(p.conv, cur, d.weight, d.bias, p.relu, out, st);
                 break;
             case CNN_LAYER_FC:
                 rc = launch_fc(cur, N, p.inC * p.inH * p.inW, d.weight, d.bias, p.outC, p.relu, out, st);
@@ -305,7 +305,19 @@ int cnn_conv2d_fwd(const float* x, int N, int C, int H, int W, const float* w, i
     ConvShape s;
     int rc = check_conv(N, C, H, W, K, R, S, sh, sw, ph, pw, groups, &s);
     if (rc) return rc;
-    return launch_conv2d(s, x, w, bias, fuse_relu != 0, y, as_stream(stream));
+    return conv2d_dispatch(s, x, w, bias, fuse_relu != 0, y, as_stream(stream));
+}
+
+int cnn_conv2d_fwd_config(const float* x, int N, int C, int H, int W, const float* w, int K, int R,
+                          int S, const float* bias, int sh, int sw, int ph, int pw, int groups,
+                          int fuse_relu, float* y, int config, cnn_stream_t stream) {
+    if ((N != 0 && (!x || !y)) || !w) return fail(CNN_ERR_INVALID, "conv: null x, w or y");
+    if (config < -1 || config >= conv2d_num_configs())
+        return fail(CNN_ERR_INVALID, "conv: no configuration %d", config);
+    ConvShape s;
+    int rc = check_conv(N, C, H, W, K, R, S, sh, sw, ph, pw, groups, &s);
+    if (rc) return rc;
+    return launch_conv2d(s, x, w, bias, fuse_relu != 0, y, as_stream(stream), config);
 }
 
 int cnn_fc_fwd(const float* x, int N, int I, const float* w, const float* bias, int O, int fuse_relu,

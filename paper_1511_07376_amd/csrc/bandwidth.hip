@@ -81,38 +81,54 @@ __global__ void __launch_bounds__(kThreads) avgpool_f32(PoolParams p) {
 }
 
 // ------------------------------------------------------------------ LRN
-// One thread per pixel column (n, h, w); it walks the channels keeping the
-// HALF values on each side of the current channel in registers, so every
-// input element is read from memory once.  Lanes cover consecutive w.
+// One thread per (n, chunk of CCH channels, pixel); lanes cover consecutive
+// pixels.  The thread walks its channels keeping the HALF values on each
+// side of the current channel in registers, so it reads each of its
+// channels once plus a halo of HALF channels on each side of the chunk.
+// Splitting the channels into chunks gives the launch enough threads to keep
+// HBM busy even for the 27x27 layers.
 struct LrnParams {
     const float* x;
     float* y;
     int C, HW;
-    int total;  // N*H*W
+    int nchunk;  // ceil(C / CCH)
+    int total;   // N * nchunk * H*W
     float alpha_over_size, beta, k;
 };
 
-template <int HALF>
+// scale^(-beta) through the hardware base-2 logarithm and exponential
+// (v_log_f32, v_exp_f32): relative error a few ulp for the scales LRN meets.
+__device__ inline float pow_neg(float scale, float beta) {
+    return __builtin_amdgcn_exp2f(-beta * __builtin_amdgcn_logf(scale));
+}
+
+template <int HALF, int CCH>
 __global__ void __launch_bounds__(kThreads) lrn_across_f32(LrnParams p) {
     constexpr int WIN = 2 * HALF + 1;
     for (int t = blockIdx.x * kThreads + threadIdx.x; t < p.total; t += gridDim.x * kThreads) {
-        const int n = t / p.HW;
-        const int hw = t - n * p.HW;
+        const int hw = t % p.HW;
+        const int rest = t / p.HW;
+        const int chunk = rest % p.nchunk;
+        const int n = rest / p.nchunk;
+        const int c0 = chunk * CCH;
         const float* xp = p.x + n * p.C * p.HW + hw;
         float* yp = p.y + n * p.C * p.HW + hw;
         // win[j] holds channel c - HALF + j (0 outside [0, C))
         float win[WIN];
 #pragma unroll
         for (int j = 0; j < WIN; ++j) {
-            const int cc = j - HALF;
+            const int cc = c0 + j - HALF;
             win[j] = (cc >= 0 && cc < p.C) ? xp[cc * p.HW] : 0.0f;
         }
-        for (int c = 0; c < p.C; ++c) {
+#pragma unroll
+        for (int i = 0; i < CCH; ++i) {
+            const int c = c0 + i;
+            if (c >= p.C) break;
             float sq = 0.0f;
 #pragma unroll
             for (int j = 0; j < WIN; ++j) sq += win[j] * win[j];
             const float scale = p.k + p.alpha_over_size * sq;
-            yp[c * p.HW] = win[HALF] * powf(scale, -p.beta);
+            yp[c * p.HW] = win[HALF] * pow_neg(scale, p.beta);
 #pragma unroll
             for (int j = 0; j < WIN - 1; ++j) win[j] = win[j + 1];
             const int cn = c + HALF + 1;
@@ -136,7 +152,7 @@ __global__ void __launch_bounds__(kThreads) lrn_across_any_f32(LrnParams p, int 
                 sq += v * v;
             }
             const float scale = p.k + p.alpha_over_size * sq;
-            yp[c * p.HW] = xp[c * p.HW] * powf(scale, -p.beta);
+            yp[c * p.HW] = xp[c * p.HW] * pow_neg(scale, p.beta);
         }
     }
 }
@@ -190,19 +206,27 @@ int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha
     p.y = y;
     p.C = C;
     p.HW = H * W;
-    p.total = N * H * W;
     p.alpha_over_size = alpha / (float)size;
     p.beta = beta;
     p.k = k;
-    if (p.total == 0) return CNN_OK;
+    if (N == 0) return CNN_OK;
+    constexpr int kChunk = 32;
+    if (size / 2 > 4) {  // wide windows: recompute each window sum
+        p.nchunk = 1;
+        p.total = N * p.HW;
+        hipLaunchKernelGGL(lrn_across_any_f32, dim3(grid_for(p.total)), dim3(kThreads), 0, st, p,
+                           size / 2);
+        return check_launch("lrn_across_any_f32");
+    }
+    p.nchunk = ceil_div(C, kChunk);
+    p.total = N * p.nchunk * p.HW;
     const dim3 grid(grid_for(p.total)), block(kThreads);
     switch (size / 2) {
-        case 0: hipLaunchKernelGGL(lrn_across_f32<0>, grid, block, 0, st, p); break;
-        case 1: hipLaunchKernelGGL(lrn_across_f32<1>, grid, block, 0, st, p); break;
-        case 2: hipLaunchKernelGGL(lrn_across_f32<2>, grid, block, 0, st, p); break;
-        case 3: hipLaunchKernelGGL(lrn_across_f32<3>, grid, block, 0, st, p); break;
-        case 4: hipLaunchKernelGGL(lrn_across_f32<4>, grid, block, 0, st, p); break;
-        default: hipLaunchKernelGGL(lrn_across_any_f32, grid, block, 0, st, p, size / 2); break;
+        case 0: hipLaunchKernelGGL((lrn_across_f32<0, kChunk>), grid, block, 0, st, p); break;
+        case 1: hipLaunchKernelGGL((lrn_across_f32<1, kChunk>), grid, block, 0, st, p); break;
+        case 2: hipLaunchKernelGGL((lrn_across_f32<2, kChunk>), grid, block, 0, st, p); break;
+        case 3: hipLaunchKernelGGL((lrn_across_f32<3, kChunk>), grid, block, 0, st, p); break;
+        default: hipLaunchKernelGGL((lrn_across_f32<4, kChunk>), grid, block, 0, st, p); break;
     }
     return check_launch("lrn_across_f32");
 }

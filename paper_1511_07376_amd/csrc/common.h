@@ -37,8 +37,16 @@ int pool_out(int H, int W, int kh, int kw, int sh, int sw, int ph, int pw, int c
 
 // Launchers: arguments already validated; they enqueue and return CNN_OK or
 // CNN_ERR_HIP.
+// cfg: index into the convolution configuration table, or -1 for the
+// built-in heuristic.
 int launch_conv2d(const ConvShape& s, const float* x, const float* w, const float* bias,
-                  int relu, float* y, hipStream_t st);
+                  int relu, float* y, hipStream_t st, int cfg);
+int conv2d_num_configs();
+const char* conv2d_config_name(int i);
+// Convolution with the tuned configuration for this shape (auto-tuning it
+// first when auto-tuning is on and the shape is new).
+int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const float* bias,
+                    int relu, float* y, hipStream_t st);
 int launch_fc(const float* x, int N, int I, const float* w, const float* bias, int O, int relu,
               float* y, hipStream_t st);
 int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y, int32_t* idx,

@@ -4,29 +4,39 @@
 //     Y_g[k][m] = sum_kk W_g[k][kk] * X_g[kk][m]      (+ bias, optional ReLU)
 // with k an output channel of the group (Kg = K/G rows), m = (n, p, q) an
 // output pixel (M = N*P*Q columns) and kk = (c, r, s) a tap of the filter
-// (Kr = (C/G)*R*S).  X_g is the im2col matrix of the input; it is never
-// built in memory: each workgroup gathers the slab of it that it needs
-// straight from the NCHW input into LDS, with zero fill for padding and for
-// tile tails.
+// (Kr = (C/G)*R*S, in the weights' own [c][r][s] order).  X_g is the im2col
+// matrix of the input; it is never built in memory: each workgroup gathers the
+// slab of it that it needs straight from the NCHW input into LDS.
+//
+// Gather: every thread owns one output pixel (fixed for the whole kernel) and
+// a run of consecutive taps per slab; the taps' (c, r, s) are wave-uniform and
+// advance in scalar registers.  Loads go through a buffer resource: a tap
+// that falls into the zero padding, or past the end of the reduction, gets an
+// out-of-range offset and the hardware returns 0, so the gather has no
+// branches.
 //
 // Workgroup tile: TM output channels x TN output pixels, reduction in slabs of
-// BK taps, double-buffered in LDS (the global loads of slab s+1 are in flight
-// while slab s feeds the matrix cores).  Each wave owns FM x FN blocks of
-// 32x32 accumulated with v_mfma_f32_32x32x2_f32.  The output channel is the
-// MFMA row and the output pixel the MFMA column, so the 32 lanes of a row
-// store 32 consecutive pixels: NCHW stores are coalesced.
+// BK taps, double-buffered in LDS (the loads of slab s+1 are in flight while
+// slab s feeds the matrix cores).  Each wave owns FM x FN blocks of 32x32
+// accumulated with v_mfma_f32_32x32x2_f32.  The output channel is the MFMA
+// row and the output pixel the MFMA column, so the 32 lanes of a row store 32
+// consecutive pixels: NCHW stores are coalesced.
 //
-// Reduction order inside a slab: lanes 0-31 of a wave take the first BK/2
-// taps of the slab and lanes 32-63 the last BK/2 (an MFMA step consumes one
-// tap per lane half), so each lane reads BK/2 consecutive LDS words per
-// fragment with 128-bit loads.  The order of a sum does not change its value
-// beyond rounding.
+// Reduction order inside a slab: lanes 0-31 take the first BK/2 taps of the
+// slab and lanes 32-63 the last BK/2 (an MFMA step consumes one tap per lane
+// half), so each lane reads BK/2 consecutive LDS words per fragment with
+// 128-bit loads.  The order of a sum changes its value only by rounding.
+#include <cstdlib>
+#include <cstring>
+
 #include "common.h"
 
 namespace cnn {
 namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kOutOfRange = (int)0x80000000u;  // buffer offset that reads as 0
 
 struct ConvParams {
     const float* x;
@@ -36,6 +46,7 @@ struct ConvParams {
     int C, H, W, K, R, S, P, Q;
     int sh, sw, ph, pw;
     int Cg, Kg, Kr, RS, HW, PQ, M;
+    int xbytes;  // bytes of x covered by this launch (< 2^31)
     int relu;
 };
 
@@ -62,12 +73,11 @@ conv2d_igemm_f32(ConvParams p) {
     const int m0 = blockIdx.x * TN;
     const int k0 = blockIdx.y * TM;
 
-    // ---- gather setup: this thread's pixel column and tap run (fixed for all slabs)
+    // ---- gather setup: this thread's pixel and tap run (fixed for all slabs)
     const int mloc = tid % TN;
     const int kgrp = __builtin_amdgcn_readfirstlane(tid / TN);  // uniform: TN >= 64
     const int m = m0 + mloc;
-    int hb, wb;
-    const float* xb;
+    int hb, wb, lane_off;
     if (m < p.M) {
         const int n = m / p.PQ;
         const int pq = m - n * p.PQ;
@@ -75,12 +85,14 @@ conv2d_igemm_f32(ConvParams p) {
         const int qq = pq - pp * p.Q;
         hb = pp * p.sh - p.ph;
         wb = qq * p.sw - p.pw;
-        xb = p.x + (n * p.C + g * p.Cg) * p.HW;
+        lane_off = ((n * p.C + g * p.Cg) * p.HW + hb * p.W + wb) * 4;
     } else {
-        hb = -0x40000000;  // every row test fails: the column is zero
+        hb = -0x40000000;  // every row test fails: the column reads as zero
         wb = 0;
-        xb = p.x;
+        lane_off = 0;
     }
+    const __amdgpu_buffer_rsrc_t xres =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.x), (short)0, p.xbytes, 0x00020000);
 
     float xr[KRUN];
     auto load_x = [&](int kslab) {
@@ -89,20 +101,23 @@ conv2d_igemm_f32(ConvParams p) {
         const int rs = kk0 - c * p.RS;
         int r = rs / p.S;
         int s = rs - r * p.S;
+        int toff = ((c * p.H + r) * p.W + s) * 4;  // byte offset of tap (c, r, s)
 #pragma unroll
         for (int j = 0; j < KRUN; ++j) {
-            const int h = hb + r;
-            const int w = wb + s;
-            const bool ok = (kk0 + j < p.Kr) && ((unsigned)h < (unsigned)p.H) &&
-                            ((unsigned)w < (unsigned)p.W);
-            xr[j] = ok ? xb[c * p.HW + h * p.W + w] : 0.0f;
-            if (++s == p.S) {
-                s = 0;
-                if (++r == p.R) {
-                    r = 0;
-                    ++c;
-                }
-            }
+            const bool ok = (kk0 + j < p.Kr) && ((unsigned)(hb + r) < (unsigned)p.H) &&
+                            ((unsigned)(wb + s) < (unsigned)p.W);
+            const int voff = ok ? lane_off + toff : kOutOfRange;
+            xr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, voff, 0, 0));
+            // next tap: s, then r, then c
+            ++s;
+            toff += 4;
+            const bool wrap_s = (s == p.S);
+            s = wrap_s ? 0 : s;
+            r += wrap_s ? 1 : 0;
+            toff += wrap_s ? (p.W - p.S) * 4 : 0;
+            const bool wrap_r = (r == p.R);
+            r = wrap_r ? 0 : r;
+            toff += wrap_r ? (p.HW - p.R * p.W) * 4 : 0;
         }
     };
     auto store_x = [&](int buf) {
@@ -245,6 +260,9 @@ conv2d_igemm_f32(ConvParams p) {
     }
 }
 
+// ---------------------------------------------------------------- configurations
+typedef int (*LaunchFn)(const ConvParams&, int G, bool vec_w, hipStream_t st);
+
 template <int WMW, int WNW, int FM, int FN, int BK>
 int launch_cfg(const ConvParams& prm, int G, bool vec_w, hipStream_t st) {
     constexpr int TM = WMW * FM * 32;
@@ -258,15 +276,59 @@ int launch_cfg(const ConvParams& prm, int G, bool vec_w, hipStream_t st) {
     return check_launch("conv2d_igemm_f32");
 }
 
+struct ConvConfig {
+    const char* name;  // "TMxTNxBK"
+    int tm, tn, bk, threads;
+    LaunchFn launch;
+};
+
+#define CNN_CONV_CFG(WMW, WNW, FM, FN, BK)                                                       \
+    ConvConfig {                                                                                \
+        #WMW "x" #WNW " waves, " #FM "x" #FN " blocks, BK " #BK, WMW * FM * 32, WNW * FN * 32, \
+            BK, 64 * WMW * WNW, &launch_cfg<WMW, WNW, FM, FN, BK>                               \
+    }
+
+const ConvConfig kConfigs[] = {
+    CNN_CONV_CFG(2, 2, 2, 2, 16),  // 0: 128 x 128
+    CNN_CONV_CFG(2, 2, 2, 2, 32),  // 1: 128 x 128
+    CNN_CONV_CFG(4, 1, 1, 2, 16),  // 2: 128 x 64
+    CNN_CONV_CFG(4, 1, 1, 2, 32),  // 3: 128 x 64
+    CNN_CONV_CFG(1, 4, 2, 1, 16),  // 4: 64 x 128
+    CNN_CONV_CFG(1, 4, 2, 1, 32),  // 5: 64 x 128
+    CNN_CONV_CFG(1, 4, 3, 1, 16),  // 6: 96 x 128
+    CNN_CONV_CFG(1, 4, 3, 1, 32),  // 7: 96 x 128
+    CNN_CONV_CFG(1, 4, 1, 1, 16),  // 8: 32 x 128
+    CNN_CONV_CFG(2, 2, 1, 1, 16),  // 9: 64 x 64
+    CNN_CONV_CFG(2, 2, 1, 1, 32),  // 10: 64 x 64
+    CNN_CONV_CFG(2, 4, 2, 2, 16),  // 11: 128 x 256 (8 waves)
+    CNN_CONV_CFG(1, 2, 3, 2, 16),  // 12: 96 x 128 (2 waves)
+    CNN_CONV_CFG(2, 1, 2, 2, 16),  // 13: 128 x 64 (2 waves)
+};
+constexpr int kNumConfigs = sizeof(kConfigs) / sizeof(kConfigs[0]);
+
+// Heuristic choice when no tuned entry exists: the output-channel tile follows
+// the group's channel count; a narrower pixel tile when the grid would leave
+// most compute units idle.
+int heuristic_config(const ConvParams& p, int G) {
+    const int mt128 = ceil_div(p.M, 128);
+    if (p.Kg <= 32) return 8;
+    if (p.Kg <= 64) return mt128 * G >= 512 ? 4 : 9;
+    if (p.Kg <= 96) return 6;
+    const int blocks = mt128 * ceil_div(p.Kg, 128) * G;
+    return blocks >= 512 ? 0 : 2;
+}
+
 }  // namespace
 
+int conv2d_num_configs() { return kNumConfigs; }
+
+const char* conv2d_config_name(int i) { return (i >= 0 && i < kNumConfigs) ? kConfigs[i].name : nullptr; }
+
 int launch_conv2d(const ConvShape& s, const float* x, const float* w, const float* bias, int relu,
-                  float* y, hipStream_t st) {
+                  float* y, hipStream_t st, int cfg) {
     ConvParams prm;
-    prm.x = x;
     prm.w = w;
     prm.bias = bias;
-    prm.y = y;
     prm.C = s.C; prm.H = s.H; prm.W = s.W; prm.K = s.K; prm.R = s.R; prm.S = s.S;
     prm.P = s.P; prm.Q = s.Q;
     prm.sh = s.sh; prm.sw = s.sw; prm.ph = s.ph; prm.pw = s.pw;
@@ -276,16 +338,30 @@ int launch_conv2d(const ConvShape& s, const float* x, const float* w, const floa
     prm.Kr = prm.Cg * prm.RS;
     prm.HW = s.H * s.W;
     prm.PQ = s.P * s.Q;
-    prm.M = s.N * prm.PQ;
     prm.relu = relu;
-    if (prm.M == 0) return CNN_OK;
+    if (s.N == 0) return CNN_OK;
     const bool vec_w = (prm.Kr % 4 == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
 
-    // Tile choice: the output-channel tile follows the group's channel count.
-    if (prm.Kg <= 32) return launch_cfg<1, 4, 1, 1, 16>(prm, s.G, vec_w, st);   // 32 x 128
-    if (prm.Kg <= 64) return launch_cfg<1, 4, 2, 1, 16>(prm, s.G, vec_w, st);   // 64 x 128
-    if (prm.Kg <= 96) return launch_cfg<1, 4, 3, 1, 16>(prm, s.G, vec_w, st);   // 96 x 128
-    return launch_cfg<2, 2, 2, 2, 16>(prm, s.G, vec_w, st);                     // 128 x 128
+    // The gather addresses x through a buffer resource with 31-bit offsets:
+    // launch fewer than 2^29 input elements at a time (whole images).
+    const int64_t img = (int64_t)s.C * prm.HW;
+    const int per_launch = (int)std::min<int64_t>(s.N, (((int64_t)1 << 29) - 1) / img);
+    if (per_launch < 1) return fail(CNN_ERR_UNSUPPORTED, "conv: one image exceeds 2^29 elements");
+    if (cfg < 0) {
+        prm.M = per_launch * prm.PQ;
+        cfg = heuristic_config(prm, s.G);
+    }
+    if (cfg >= kNumConfigs) return fail(CNN_ERR_UNSUPPORTED, "conv: no configuration %d", cfg);
+    for (int n0 = 0; n0 < s.N; n0 += per_launch) {
+        const int nb = std::min(per_launch, s.N - n0);
+        prm.x = x + (size_t)n0 * img;
+        prm.y = y + (size_t)n0 * s.K * prm.PQ;
+        prm.M = nb * prm.PQ;
+        prm.xbytes = (int)(nb * img * 4);
+        const int rc = kConfigs[cfg].launch(prm, s.G, vec_w, st);
+        if (rc != CNN_OK) return rc;
+    }
+    return CNN_OK;
 }
 
 }  // namespace cnn

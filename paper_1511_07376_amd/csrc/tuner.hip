@@ -1,0 +1,159 @@
+// Auto-tuner for the convolution kernels.
+//
+// The paper's library exposes tuning parameters that set how much work each
+// GPU thread and each SIMD unit gets; when auto-tuning is switched on, the
+// first launch runs predefined scenarios, times them and keeps the fastest
+// for later runs (Sec. 3.6).  Here the tuning parameters are the
+// convolution's tile configuration (output channels x pixels per workgroup,
+// reduction slab, waves per workgroup).  With auto-tuning on, the first call
+// of each new convolution shape runs every configuration on the caller's own
+// buffers and stream, times each with HIP events, and records the fastest;
+// later calls of that shape use it.  The table can be exported as text and
+// imported again, so the search runs once per machine.
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <tuple>
+
+#include "common.h"
+
+namespace cnn {
+namespace {
+
+typedef std::tuple<int, int, int, int, int, int, int, int, int, int, int, int> Key;
+
+Key key_of(const ConvShape& s) {
+    return Key(s.N, s.C, s.H, s.W, s.K, s.R, s.S, s.sh, s.sw, s.ph, s.pw, s.G);
+}
+
+std::mutex g_mu;
+std::map<Key, int> g_table;  // shape -> configuration index
+int g_autotune = 0;
+
+constexpr int kTimedRuns = 3;
+
+// Times every configuration on this shape; returns the fastest, or -1.
+int tune(const ConvShape& s, const float* x, const float* w, const float* bias, int relu, float* y,
+         hipStream_t st) {
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone) return -1;
+    hipEvent_t e0, e1;
+    if (hipEventCreate(&e0) != hipSuccess) return -1;
+    if (hipEventCreate(&e1) != hipSuccess) {
+        hipEventDestroy(e0);
+        return -1;
+    }
+    int best = -1;
+    float best_ms = 0.0f;
+    for (int c = 0; c < conv2d_num_configs(); ++c) {
+        if (launch_conv2d(s, x, w, bias, relu, y, st, c) != CNN_OK) continue;  // warm-up run
+        hipEventRecord(e0, st);
+        for (int r = 0; r < kTimedRuns; ++r) launch_conv2d(s, x, w, bias, relu, y, st, c);
+        hipEventRecord(e1, st);
+        if (hipEventSynchronize(e1) != hipSuccess) break;
+        float ms = 0.0f;
+        if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) continue;
+        if (best < 0 || ms < best_ms) {
+            best = c;
+            best_ms = ms;
+        }
+    }
+    hipEventDestroy(e0);
+    hipEventDestroy(e1);
+    (void)hipGetLastError();
+    return best;
+}
+
+}  // namespace
+
+int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const float* bias, int relu,
+                    float* y, hipStream_t st) {
+    int cfg = -1;
+    bool autotune;
+    {
+        std::lock_guard<std::mutex> lock(g_mu);
+        auto it = g_table.find(key_of(s));
+        if (it != g_table.end()) cfg = it->second;
+        autotune = g_autotune != 0;
+    }
+    if (cfg < 0 && autotune && s.N > 0) {
+        cfg = tune(s, x, w, bias, relu, y, st);
+        if (cfg >= 0) {
+            std::lock_guard<std::mutex> lock(g_mu);
+            g_table[key_of(s)] = cfg;
+        }
+    }
+    return launch_conv2d(s, x, w, bias, relu, y, st, cfg);
+}
+
+}  // namespace cnn
+
+using namespace cnn;
+
+extern "C" {
+
+int cnn_set_autotune(int mode) {
+    if (mode != 0 && mode != 1) return fail(CNN_ERR_INVALID, "set_autotune: mode %d", mode);
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_autotune = mode;
+    return CNN_OK;
+}
+
+int cnn_conv2d_num_configs(void) { return conv2d_num_configs(); }
+
+const char* cnn_conv2d_config_name(int i) { return conv2d_config_name(i); }
+
+size_t cnn_tuning_export(char* buf, size_t cap) {
+    std::string out;
+    {
+        std::lock_guard<std::mutex> lock(g_mu);
+        for (const auto& kv : g_table) {
+            const Key& k = kv.first;
+            char line[160];
+            snprintf(line, sizeof(line), "%d %d %d %d %d %d %d %d %d %d %d %d %d\n", std::get<0>(k),
+                     std::get<1>(k), std::get<2>(k), std::get<3>(k), std::get<4>(k), std::get<5>(k),
+                     std::get<6>(k), std::get<7>(k), std::get<8>(k), std::get<9>(k), std::get<10>(k),
+                     std::get<11>(k), kv.second);
+            out += line;
+        }
+    }
+    if (buf && cap > 0) {
+        const size_t n = std::min(cap - 1, out.size());
+        memcpy(buf, out.data(), n);
+        buf[n] = '\0';
+    }
+    return out.size() + 1;
+}
+
+int cnn_tuning_import(const char* text) {
+    if (!text) return fail(CNN_ERR_INVALID, "tuning_import: null text");
+    int count = 0;
+    const char* p = text;
+    while (*p) {
+        const char* eol = strchr(p, '\n');
+        const size_t len = eol ? (size_t)(eol - p) : strlen(p);
+        std::string line(p, len);
+        p += len + (eol ? 1 : 0);
+        if (line.empty() || line[0] == '#') continue;
+        int v[13];
+        if (sscanf(line.c_str(), "%d %d %d %d %d %d %d %d %d %d %d %d %d", &v[0], &v[1], &v[2], &v[3],
+                   &v[4], &v[5], &v[6], &v[7], &v[8], &v[9], &v[10], &v[11], &v[12]) != 13)
+            return fail(CNN_ERR_INVALID, "tuning_import: bad line '%s'", line.c_str());
+        if (v[12] < 0 || v[12] >= conv2d_num_configs())
+            return fail(CNN_ERR_INVALID, "tuning_import: no configuration %d", v[12]);
+        std::lock_guard<std::mutex> lock(g_mu);
+        g_table[Key(v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7], v[8], v[9], v[10], v[11])] = v[12];
+        ++count;
+    }
+    return count;
+}
+
+int cnn_tuning_clear(void) {
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_table.clear();
+    return CNN_OK;
+}
+
+}  // extern "C"

@@ -173,3 +173,25 @@ def test_net_rejects_before_launch():
     assert L.cnn_net_fwd(descs, n, FAKE, 2, 4, H, W, FAKE, FAKE, 1 << 40, 0) == cnn.CNN_ERR_INVALID
     assert L.cnn_net_fwd_timed(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, None, 0) == cnn.CNN_ERR_INVALID
     assert L.cnn_net_workspace_bytes(descs, 0, 2, C, H, W) == 0
+
+
+def test_tuning_table_text_roundtrip():
+    """Import / export / clear of the tuning records: host-only, no launches."""
+    assert cnn.cnn_conv2d_num_configs() >= 4
+    assert cnn.cnn_conv2d_config_name(0)
+    assert cnn.cnn_conv2d_config_name(-5) is None
+    cnn.cnn_tuning_clear()
+    assert cnn.cnn_tuning_export() == ""
+    n = cnn.cnn_tuning_import("# comment\n64 3 227 227 96 11 11 4 4 0 0 1 2\n64 256 13 13 384 3 3 1 1 1 1 1 0\n")
+    assert n == 2
+    text = cnn.cnn_tuning_export()
+    assert "64 3 227 227 96 11 11 4 4 0 0 1 2\n" in text and text.count("\n") == 2
+    with pytest.raises(cnn.CnnError):
+        cnn.cnn_tuning_import("1 2 3\n")
+    with pytest.raises(cnn.CnnError):
+        cnn.cnn_tuning_import(f"1 3 8 8 4 3 3 1 1 0 0 1 {cnn.cnn_conv2d_num_configs()}\n")
+    assert L.cnn_set_autotune(7) == cnn.CNN_ERR_INVALID
+    assert L.cnn_conv2d_fwd_config(FAKE, 1, 3, 8, 8, FAKE, 4, 3, 3, 0, 1, 1, 0, 0, 1, 0, FAKE, 999, 0) \
+        == cnn.CNN_ERR_INVALID
+    cnn.cnn_tuning_clear()
+    assert cnn.cnn_tuning_export() == ""

@@ -270,3 +270,49 @@ def test_binding_errors(gpu):
         gpu.cnn_relu_fwd(torch.zeros(4, device="cuda", dtype=torch.float64))
     with pytest.raises(gpu.CnnError):
         gpu.cnn_lrn_fwd(x, size=4)
+
+
+# ---------------------------------------------------------------- every tile configuration
+CFG_SHAPES = [
+    # N, C, H, W, K, R, S, stride, pad, G
+    (2, 5, 13, 11, 70, 3, 3, 1, 1, 1),
+    (3, 6, 17, 19, 130, 5, 5, 2, 2, 2),
+    (1, 3, 31, 29, 97, 11, 11, 4, 0, 1),
+]
+
+
+@pytest.mark.parametrize("shape", CFG_SHAPES, ids=[f"shape{i}" for i in range(len(CFG_SHAPES))])
+def test_conv_every_config(gpu, shape):
+    N, C, H, W, K, R, S, st, pd, G = shape
+    x = wl.normal((N, C, H, W), 1.0, 20, 0)
+    w = wl.normal((K, C // G, R, S), 1.0, 20, 1)
+    b = wl.normal((K,), 1.0, 20, 2)
+    ref = oracle.conv2d_fwd(x, w, b, (st, st), (pd, pd), G, True)
+    xd, wd, bd = to_dev(x), to_dev(w), to_dev(b)
+    for cfg in range(-1, gpu.cnn_conv2d_num_configs()):
+        print(f"conv config {cfg} ({gpu.cnn_conv2d_config_name(cfg)}) shape {shape}", flush=True)
+        y = gpu.cnn_conv2d_fwd(xd, wd, bd, st, pd, G, True, config=cfg)
+        assert_gemm_close(to_host(y), ref, (C // G) * R * S, f"config {cfg}")
+
+
+def test_autotune_records_and_reuses(gpu):
+    shape = (4, 16, 14, 14, 96, 3, 3, 1, 1, 1)
+    N, C, H, W, K, R, S, st, pd, G = shape
+    x = wl.normal((N, C, H, W), 1.0, 21, 0)
+    w = wl.normal((K, C, R, S), 1.0, 21, 1)
+    ref = oracle.conv2d_fwd(x, w, None, (st, st), (pd, pd), G, False)
+    gpu.cnn_tuning_clear()
+    gpu.cnn_set_autotune(True)
+    try:
+        y = gpu.cnn_conv2d_fwd(to_dev(x), to_dev(w), None, st, pd, G, False)
+        assert_gemm_close(to_host(y), ref, C * R * S, "autotuned call")
+    finally:
+        gpu.cnn_set_autotune(False)
+    text = gpu.cnn_tuning_export()
+    lines = [l for l in text.splitlines() if l.startswith("4 16 14 14 96 3 3 1 1 1 1 1 ")]
+    assert len(lines) == 1, text
+    cfg = int(lines[0].split()[-1])
+    assert 0 <= cfg < gpu.cnn_conv2d_num_configs()
+    y = gpu.cnn_conv2d_fwd(to_dev(x), to_dev(w), None, st, pd, G, False)   # uses the record
+    assert_gemm_close(to_host(y), ref, C * R * S, "tuned record")
+    gpu.cnn_tuning_clear()
