@@ -47,8 +47,27 @@ struct ConvParams {
     int sh, sw, ph, pw;
     int Cg, Kg, Kr, RS, HW, PQ, M;
     int xbytes;  // bytes of x covered by this launch (< 2^31)
+    int wbytes;  // bytes of w (< 2^31)
     int relu;
 };
+
+// Instruction-scheduling pattern of one slab (LLVM sched_group_barrier masks:
+// 0x008 matrix core, 0x100 LDS read, 0x020 memory read, 0x002 vector ALU,
+// 0x004 scalar ALU, 0x200 LDS write): the fragment reads first, then each
+// matrix-core instruction followed by a share of the next slab's loads and
+// address arithmetic, then the LDS writes.
+template <int NMFMA, int NDSREAD, int NVMEM>
+__device__ inline void schedule_slab() {
+    __builtin_amdgcn_sched_group_barrier(0x100, NDSREAD, 0);
+#pragma unroll
+    for (int i = 0; i < NMFMA; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (i < NVMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x004, 5, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x200, 16, 0);
+}
 
 template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W>
 __global__ void __launch_bounds__(64 * WMW * WNW)
@@ -63,9 +82,10 @@ conv2d_igemm_f32(ConvParams p) {
     static_assert(BK % KGROUPS == 0 && KRUN % 4 == 0, "gather run must be whole float4s");
     static_assert(BK % 8 == 0, "slab must split into two halves of float4s");
     constexpr int WTOT = VEC_W ? TM * BK / 4 : TM * BK;  // weight-tile loads per slab
-    constexpr int WV = (WTOT + NT - 1) / NT;                // ... per thread (last one guarded)
+    constexpr int WV = (WTOT + NT - 1) / NT;                // ... per thread
+    constexpr int AROWS = WV * NT / (VEC_W ? BK / 4 : BK);  // TM rows + spare rows
 
-    __shared__ __attribute__((aligned(16))) float sA[2][TM * LDK];  // weights  [k][kk]
+    __shared__ __attribute__((aligned(16))) float sA[2][AROWS * LDK];  // weights  [k][kk]
     __shared__ __attribute__((aligned(16))) float sB[2][TN * LDK];  // im2col   [m][kk]
 
     const int tid = threadIdx.x;
@@ -127,44 +147,54 @@ conv2d_igemm_f32(ConvParams p) {
             *reinterpret_cast<float4*>(dst + j) = make_float4(xr[j], xr[j + 1], xr[j + 2], xr[j + 3]);
     };
 
-    // ---- weight tile loads: rows k0.. of the group's [Kg][Kr] block
-    const float* wg = p.w + g * p.Kg * p.Kr;
-    float4 wr4[VEC_W ? WV : 1];
-    float wr1[VEC_W ? 1 : WV];
+    // ---- weight tile loads: rows k0.. of the group's [Kg][Kr] block, through a
+    // buffer resource as well (rows past the group or taps past the reduction
+    // read as zero).  Items past the tile land in spare LDS rows never read.
+    const __amdgpu_buffer_rsrc_t wres =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.w), (short)0, p.wbytes, 0x00020000);
+    constexpr int VW = VEC_W ? 4 : 1;
+    int w_off[WV], w_col[WV], w_lds[WV];
+    bool w_rowok[WV];
+#pragma unroll
+    for (int i = 0; i < WV; ++i) {
+        const int idx = tid + i * NT;
+        const int row = idx / (BK / VW);
+        w_col[i] = (idx % (BK / VW)) * VW;
+        w_rowok[i] = row < TM && k0 + row < p.Kg;
+        w_off[i] = w_rowok[i] ? ((g * p.Kg + k0 + row) * p.Kr + w_col[i]) * 4 : 0;
+        w_lds[i] = row * LDK + w_col[i];
+    }
+    float wr[WV * VW];
     auto load_w = [&](int kslab) {
 #pragma unroll
         for (int i = 0; i < WV; ++i) {
-            const int idx = tid + i * NT;
-            if (WTOT % NT != 0 && idx >= WTOT) break;
             if constexpr (VEC_W) {
-                const int row = idx / (BK / 4);
-                const int col = (idx % (BK / 4)) * 4;
-                const int kr = k0 + row, kk = kslab + col;
-                wr4[i] = (kr < p.Kg && kk < p.Kr)
-                             ? *reinterpret_cast<const float4*>(wg + kr * p.Kr + kk)
-                             : make_float4(0.f, 0.f, 0.f, 0.f);
+                const bool ok = w_rowok[i] && (kslab + w_col[i] < p.Kr);
+                const int voff = ok ? w_off[i] + kslab * 4 : kOutOfRange;
+                // Cast the whole vector: a bit-cast of one element of an
+                // ext_vector lvalue reads element 0 with this compiler.
+                typedef float f32x4 __attribute__((ext_vector_type(4)));
+                const f32x4 v =
+                    __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(wres, voff, 0, 0));
+                wr[4 * i] = v[0];
+                wr[4 * i + 1] = v[1];
+                wr[4 * i + 2] = v[2];
+                wr[4 * i + 3] = v[3];
             } else {
-                const int row = idx / BK;
-                const int col = idx % BK;
-                const int kr = k0 + row, kk = kslab + col;
-                wr1[i] = (kr < p.Kg && kk < p.Kr) ? wg[kr * p.Kr + kk] : 0.0f;
+                const bool ok = w_rowok[i] && (kslab + w_col[i] < p.Kr);
+                const int voff = ok ? w_off[i] + kslab * 4 : kOutOfRange;
+                wr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wres, voff, 0, 0));
             }
         }
     };
     auto store_w = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < WV; ++i) {
-            const int idx = tid + i * NT;
-            if (WTOT % NT != 0 && idx >= WTOT) break;
-            if constexpr (VEC_W) {
-                const int row = idx / (BK / 4);
-                const int col = (idx % (BK / 4)) * 4;
-                *reinterpret_cast<float4*>(&sA[buf][row * LDK + col]) = wr4[i];
-            } else {
-                const int row = idx / BK;
-                const int col = idx % BK;
-                sA[buf][row * LDK + col] = wr1[i];
-            }
+            if constexpr (VEC_W)
+                *reinterpret_cast<float4*>(&sA[buf][w_lds[i]]) =
+                    make_float4(wr[4 * i], wr[4 * i + 1], wr[4 * i + 2], wr[4 * i + 3]);
+            else
+                sA[buf][w_lds[i]] = wr[i];
         }
     };
 
@@ -214,6 +244,11 @@ conv2d_igemm_f32(ConvParams p) {
     };
 
     // ---- main loop: slab s computes from LDS while slab s+1 loads from memory
+    // The body is one basic block: the last iteration loads a slab past the
+    // reduction (all zeros) into the idle buffer, which nothing reads.  The
+    // scheduling hints spread the next slab's loads and address arithmetic
+    // between the matrix-core instructions of the current slab, so that the
+    // wave keeps issuing while the matrix core works.
     const int nslab = (p.Kr + BK - 1) / BK;
     load_x(0);
     load_w(0);
@@ -222,16 +257,12 @@ conv2d_igemm_f32(ConvParams p) {
     __syncthreads();
     for (int sl = 0; sl < nslab; ++sl) {
         const int cur = sl & 1;
-        const bool more = sl + 1 < nslab;
-        if (more) {
-            load_x((sl + 1) * BK);
-            load_w((sl + 1) * BK);
-        }
+        load_x((sl + 1) * BK);
+        load_w((sl + 1) * BK);
         compute(cur);
-        if (more) {
-            store_x(cur ^ 1);
-            store_w(cur ^ 1);
-        }
+        store_x(cur ^ 1);
+        store_w(cur ^ 1);
+        schedule_slab<FM * FN * (BK / 2), (FM + FN) * (BK / 8), KRUN + WV>();
         __syncthreads();
     }
 
@@ -341,6 +372,9 @@ int launch_conv2d(const ConvShape& s, const float* x, const float* w, const floa
     prm.relu = relu;
     if (s.N == 0) return CNN_OK;
     const bool vec_w = (prm.Kr % 4 == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
+    const int64_t wbytes = (int64_t)s.K * prm.Kr * 4;
+    if (wbytes >= ((int64_t)1 << 31)) return fail(CNN_ERR_UNSUPPORTED, "conv: weights exceed 2 GiB");
+    prm.wbytes = (int)wbytes;
 
     // The gather addresses x through a buffer resource with 31-bit offsets:
     // launch fewer than 2^29 input elements at a time (whole images).

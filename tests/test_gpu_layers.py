@@ -275,6 +275,9 @@ def test_binding_errors(gpu):
 # ---------------------------------------------------------------- every tile configuration
 CFG_SHAPES = [
     # N, C, H, W, K, R, S, stride, pad, G
+    # reductions divisible by 4 (128-bit weight loads) and not (32-bit loads)
+    (2, 8, 12, 13, 70, 3, 3, 1, 1, 1),
+    (2, 32, 9, 9, 130, 1, 1, 1, 0, 2),
     (2, 5, 13, 11, 70, 3, 3, 1, 1, 1),
     (3, 6, 17, 19, 130, 5, 5, 2, 2, 2),
     (1, 3, 31, 29, 97, 11, 11, 4, 0, 1),
