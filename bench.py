@@ -122,7 +122,20 @@ def main():
                     help="seconds of oracle work for the CPU baseline (0 disables it)")
     ap.add_argument("--no-autotune", dest="autotune", action="store_false",
                     help="use the built-in tile heuristic instead of tuning during warm-up")
+    ap.add_argument("--tuning-file", default=None,
+                    help="import this conv tuning table before warm-up (no tuning runs for its shapes)")
+    ap.add_argument("--save-tuning", default=None, help="write the tuning table here afterwards")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
     args = ap.parse_args()
+    if args.copy_probe:
+        import torch
+        a = torch.ones(args.copy_probe * (1 << 20) // 4, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": a.numel() * 4}), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the images of a batch are independent: on N GPUs each would run batch/N)",
@@ -145,11 +158,17 @@ def main():
     # The auto-tuner (the paper's first-launch tuning, Sec. 3.6) picks each conv
     # layer's tile configuration during the first warm-up step; the timed steps
     # use the recorded choices.
+    if args.tuning_file and os.path.exists(args.tuning_file):
+        with open(args.tuning_file) as f:
+            cnn.cnn_tuning_import(f.read())
     if args.autotune:
         cnn.cnn_set_autotune(True)
     for _ in range(max(args.warmup, 1 if args.autotune else 0)):
         model(xd, y=yd)
     cnn.cnn_set_autotune(False)
+    if args.save_tuning:
+        with open(args.save_tuning, "w") as f:
+            f.write(cnn.cnn_tuning_export())
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(nl + 1)] for _ in range(args.steps)]
     for evs in events:
         for e in evs:
