@@ -125,6 +125,8 @@ def main():
     ap.add_argument("--tuning-file", default=None,
                     help="import this conv tuning table before warm-up (no tuning runs for its shapes)")
     ap.add_argument("--save-tuning", default=None, help="write the tuning table here afterwards")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the steps as replays of a captured HIP graph")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -174,13 +176,36 @@ def main():
         for e in evs:
             e.record()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    graph = None
+    if args.graph:
+        # one forward pass captured as a HIP graph and replayed per step
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            model(xd, y=yd)
+        graph.replay()
+        torch.cuda.synchronize()
+
+    # timed region: K steps, per-layer HIP events recorded between the layers
     torch.cuda.synchronize()
     start.record()
     for k in range(args.steps):
         model(xd, y=yd, events=events[k])
     end.record()
     torch.cuda.synchronize()
-    ms_step = start.elapsed_time(end) / args.steps
+    ms_step_events = start.elapsed_time(end) / args.steps
+    # the same K steps without per-layer events (and as graph replays with --graph)
+    torch.cuda.synchronize()
+    start.record()
+    for k in range(args.steps):
+        if graph is not None:
+            graph.replay()
+        else:
+            model(xd, y=yd)
+    end.record()
+    torch.cuda.synchronize()
+    ms_step_plain = start.elapsed_time(end) / args.steps
+    ms_step = ms_step_events
     assert torch.isfinite(yd).all().item(), "non-finite output"
 
     layer_ms = [float(np.mean([events[k][i].elapsed_time(events[k][i + 1]) for k in range(args.steps)]))
@@ -237,6 +262,8 @@ def main():
         "conv_gflops": round(conv_tf * 1e3, 1),
         "conv_frac_fp32_mfma_peak": round(conv_tf / PEAK_FP32_MFMA_TFLOPS, 4),
         "conv_ms": round(conv_ms, 5),
+        "ms_per_step_no_layer_events": round(ms_step_plain, 4),
+        "graph_replay": bool(graph is not None),
         "autotune": bool(args.autotune),
         "conv_configs": {" ".join(l.split()[:-1]): cnn.cnn_conv2d_config_name(int(l.split()[-1]))
                          for l in cnn.cnn_tuning_export().splitlines()},

@@ -9,8 +9,9 @@
 // slab of it that it needs straight from the NCHW input into LDS.
 //
 // Gather: every thread owns one output pixel (fixed for the whole kernel) and
-// a run of consecutive taps per slab; the taps' (c, r, s) are wave-uniform and
-// advance in scalar registers.  Loads go through a buffer resource: a tap
+// a run of consecutive taps per slab, whose (c, r, s) are wave-uniform: read
+// from a per-workgroup tap table in LDS for filters of at most 31 taps, else
+// advanced in scalar registers.  Loads go through a buffer resource: a tap
 // that falls into the zero padding, or past the end of the reduction, gets an
 // out-of-range offset and the hardware returns 0, so the gather has no
 // branches.
@@ -69,7 +70,14 @@ __device__ inline void schedule_slab() {
     __builtin_amdgcn_sched_group_barrier(0x200, 16, 0);
 }
 
-template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W>
+// TAB: filters of at most 31 taps (R*S <= 31) gather through a tap table in
+// LDS, built once per workgroup: entry kk = (byte offset of tap kk within an
+// image group) << 5 | (r*S + s); a tap index of 31 marks "past the
+// reduction".  Each thread also builds, once, a 32-bit mask of the (r, s)
+// taps that fall outside the image for its pixel (bit 31 always set).  A
+// gathered element then costs a mask bit test, an add and an OR of the
+// out-of-range bit into the buffer offset.
+template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W, bool TAB>
 __global__ void __launch_bounds__(64 * WMW * WNW)
 conv2d_igemm_f32(ConvParams p) {
     constexpr int TM = WMW * FM * 32;  // output channels per workgroup
@@ -114,9 +122,49 @@ conv2d_igemm_f32(ConvParams p) {
     const __amdgpu_buffer_rsrc_t xres =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.x), (short)0, p.xbytes, 0x00020000);
 
+    const int nslab = (p.Kr + BK - 1) / BK;
+    extern __shared__ __attribute__((aligned(16))) int stab[];  // TAB only: (nslab + 1) * BK entries
+    unsigned inv = 0xffffffffu;
+    if constexpr (TAB) {
+        for (int kk = tid; kk < (nslab + 1) * BK; kk += NT) {
+            int e = 31;
+            if (kk < p.Kr) {
+                const int c = kk / p.RS;
+                const int rs = kk - c * p.RS;
+                const int r = rs / p.S;
+                const int s = rs - r * p.S;
+                e = ((((c * p.H + r) * p.W + s) * 4) << 5) | rs;
+            }
+            stab[kk] = e;
+        }
+        if (m < p.M) {
+            inv = 0x80000000u;
+            for (int r = 0; r < p.R; ++r)
+                for (int s = 0; s < p.S; ++s)
+                    if ((unsigned)(hb + r) >= (unsigned)p.H || (unsigned)(wb + s) >= (unsigned)p.W)
+                        inv |= 1u << (r * p.S + s);
+        }
+        __syncthreads();
+    }
+
     float xr[KRUN];
     auto load_x = [&](int kslab) {
         const int kk0 = kslab + kgrp * KRUN;  // uniform
+        if constexpr (TAB) {
+#pragma unroll
+            for (int j = 0; j < KRUN; j += 4) {
+                const int4 e4 = *reinterpret_cast<const int4*>(&stab[kk0 + j]);
+                const int es[4] = {e4.x, e4.y, e4.z, e4.w};
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const unsigned bad = (inv >> (es[u] & 31)) & 1u;
+                    const int voff = (lane_off + (int)((unsigned)es[u] >> 5)) | (int)(bad << 31);
+                    xr[j + u] =
+                        __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, voff, 0, 0));
+                }
+            }
+            return;
+        }
         int c = kk0 / p.RS;
         const int rs = kk0 - c * p.RS;
         int r = rs / p.S;
@@ -249,7 +297,6 @@ conv2d_igemm_f32(ConvParams p) {
     // scheduling hints spread the next slab's loads and address arithmetic
     // between the matrix-core instructions of the current slab, so that the
     // wave keeps issuing while the matrix core works.
-    const int nslab = (p.Kr + BK - 1) / BK;
     load_x(0);
     load_w(0);
     store_x(0);
@@ -300,10 +347,19 @@ int launch_cfg(const ConvParams& prm, int G, bool vec_w, hipStream_t st) {
     constexpr int TN = WNW * FN * 32;
     dim3 grid(ceil_div(prm.M, TN), ceil_div(prm.Kg, TM), G);
     dim3 block(64 * WMW * WNW);
-    if (vec_w)
-        hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, true>), grid, block, 0, st, prm);
+    // tap table: R*S <= 31, byte offsets below 2^27, at most 32 KiB of LDS
+    const int tab_entries = (ceil_div(prm.Kr, BK) + 1) * BK;
+    const bool tab = prm.RS <= 31 && (int64_t)prm.Cg * prm.HW * 4 < ((int64_t)1 << 27) &&
+                     tab_entries * 4 <= 32768;
+    const size_t shm = tab ? (size_t)tab_entries * 4 : 0;
+    if (vec_w && tab)
+        hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, true, true>), grid, block, shm, st, prm);
+    else if (vec_w)
+        hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, true, false>), grid, block, 0, st, prm);
+    else if (tab)
+        hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, false, true>), grid, block, shm, st, prm);
     else
-        hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, false>), grid, block, 0, st, prm);
+        hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, false, false>), grid, block, 0, st, prm);
     return check_launch("conv2d_igemm_f32");
 }
 
