@@ -1,0 +1,424 @@
+// Convolution layer as an implicit GEMM on the fp32 matrix cores of gfx950.
+//
+// Per group g the layer is the product
+//     Y_g[k][m] = sum_kk W_g[k][kk] * X_g[kk][m]      (+ bias, optional ReLU)
+// with k an output channel of the group (Kg = K/G rows), m = (n, p, q) an
+// output pixel (M = N*P*Q columns) and kk = (c, r, s) a tap of the filter
+// (Kr = (C/G)*R*S, in the weights' own [c][r][s] order).  X_g is the im2col
+// matrix of the input; it is never built in memory: each workgroup gathers the
+// slab of it that it needs straight from the NCHW input into LDS.
+//
+// Gather: every thread owns one output pixel (fixed for the whole kernel) and
+// a run of consecutive taps per slab, whose (c, r, s) are wave-uniform: read
+// from a per-workgroup tap table in LDS for filters of at most 31 taps, else
+// advanced in scalar registers.  Loads go through a buffer resource: a tap
+// that falls into the zero padding, or past the end of the reduction, gets an
+// out-of-range offset and the hardware returns 0, so the gather has no
+// branches.
+//
+// Workgroup tile: TM output channels x TN output pixels, reduction in slabs of
+// BK taps, double-buffered in LDS (the loads of slab s+1 are in flight while
+// slab s feeds the matrix cores).  Each wave owns FM x FN blocks of 32x32
+// accumulated with v_mfma_f32_32x32x2_f32.  The output channel is the MFMA
+// row and the output pixel the MFMA column, so the 32 lanes of a row store 32
+// consecutive pixels: NCHW stores are coalesced.
+//
+// Reduction order inside a slab: lanes 0-31 take the first BK/2 taps of the
+// slab and lanes 32-63 the last BK/2 (an MFMA step consumes one tap per lane
+// half), so each lane reads BK/2 consecutive LDS words per fragment with
+// 128-bit loads.  The order of a sum changes its value only by rounding.
+#pragma once
+
+#include <cstdlib>
+#include <cstring>
+
+#include "common.h"
+
+namespace cnn {
+namespace conv {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kOutOfRange = (int)0x80000000u;  // buffer offset that reads as 0
+
+struct ConvParams {
+    const float* x;
+    const float* w;
+    const float* bias;
+    float* y;
+    int C, H, W, K, R, S, P, Q;
+    int sh, sw, ph, pw;
+    int Cg, Kg, Kr, RS, HW, PQ, M;
+    int xbytes;  // bytes of x covered by this launch (< 2^31)
+    int wbytes;  // bytes of w (< 2^31)
+    int relu;
+};
+
+// Instruction-scheduling pattern of one slab (LLVM sched_group_barrier masks:
+// 0x008 matrix core, 0x100 LDS read, 0x020 memory read, 0x002 vector ALU,
+// 0x004 scalar ALU, 0x200 LDS write): the fragment reads first, then each
+// matrix-core instruction followed by a share of the next slab's loads and
+// address arithmetic, then the LDS writes.
+template <int NMFMA, int NDSREAD, int NVMEM>
+__device__ inline void schedule_slab() {
+    __builtin_amdgcn_sched_group_barrier(0x100, NDSREAD, 0);
+#pragma unroll
+    for (int i = 0; i < NMFMA; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (i < NVMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x004, 5, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x200, 16, 0);
+}
+
+// Gather modes.
+//  kGatherScalar: taps decoded and advanced in scalar registers, bounds
+//    tested per element (any filter).
+//  kGatherMask: filters of at most 31 taps.  A tap table in LDS, built once
+//    per workgroup, holds entry kk = (byte offset of tap kk within an image
+//    group) << 5 | (r*S + s); tap index 31 marks "past the reduction".  Each
+//    thread builds once a 32-bit mask of the (r, s) taps that fall outside
+//    the image for its pixel (bit 31 always set).  An element costs a mask
+//    bit test, an add and an OR of the out-of-range bit into the offset.
+//  kGatherNoPad: no padding, so every tap of an in-range pixel lies inside
+//    the image.  The table holds byte offsets (2^31 past the reduction) and
+//    out-of-range pixels start at 2^31: an element costs one add.
+constexpr int kGatherScalar = 0, kGatherMask = 1, kGatherNoPad = 2;
+
+template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W, int GATHER>
+__global__ void __launch_bounds__(64 * WMW * WNW)
+conv2d_igemm_f32(ConvParams p) {
+    constexpr int TM = WMW * FM * 32;  // output channels per workgroup
+    constexpr int TN = WNW * FN * 32;  // output pixels per workgroup
+    constexpr int NT = 64 * WMW * WNW;
+    constexpr int LDK = BK + 4;        // padded LDS row (conflict-free 128-bit reads)
+    constexpr int KGROUPS = NT / TN;   // threads sharing one pixel column of the gather
+    constexpr int KRUN = BK / KGROUPS; // consecutive taps gathered per thread
+    static_assert(NT % TN == 0 && TN >= 64, "gather layout needs TN | NT and TN >= 64");
+    static_assert(BK % KGROUPS == 0 && KRUN % 4 == 0, "gather run must be whole float4s");
+    static_assert(BK % 8 == 0, "slab must split into two halves of float4s");
+    constexpr int WTOT = VEC_W ? TM * BK / 4 : TM * BK;  // weight-tile loads per slab
+    constexpr int WV = (WTOT + NT - 1) / NT;                // ... per thread
+    constexpr int AROWS = WV * NT / (VEC_W ? BK / 4 : BK);  // TM rows + spare rows
+
+    __shared__ __attribute__((aligned(16))) float sA[2][AROWS * LDK];  // weights  [k][kk]
+    __shared__ __attribute__((aligned(16))) float sB[2][TN * LDK];  // im2col   [m][kk]
+
+    const int tid = threadIdx.x;
+    const int g = blockIdx.z;
+    const int m0 = blockIdx.x * TN;
+    const int k0 = blockIdx.y * TM;
+
+    // ---- gather setup: this thread's pixel and tap run (fixed for all slabs)
+    const int mloc = tid % TN;
+    const int kgrp = __builtin_amdgcn_readfirstlane(tid / TN);  // uniform: TN >= 64
+    const int m = m0 + mloc;
+    int hb, wb, lane_off;
+    if (m < p.M) {
+        const int n = m / p.PQ;
+        const int pq = m - n * p.PQ;
+        const int pp = pq / p.Q;
+        const int qq = pq - pp * p.Q;
+        hb = pp * p.sh - p.ph;
+        wb = qq * p.sw - p.pw;
+        lane_off = ((n * p.C + g * p.Cg) * p.HW + hb * p.W + wb) * 4;
+    } else {
+        hb = -0x40000000;  // every row test fails: the column reads as zero
+        wb = 0;
+        lane_off = 0;
+    }
+    const __amdgpu_buffer_rsrc_t xres =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.x), (short)0, p.xbytes, 0x00020000);
+
+    const int nslab = (p.Kr + BK - 1) / BK;
+    extern __shared__ __attribute__((aligned(16))) int stab[];  // (nslab + 1) * BK entries
+    unsigned inv = 0xffffffffu;
+    if constexpr (GATHER != kGatherScalar) {
+        for (int kk = tid; kk < (nslab + 1) * BK; kk += NT) {
+            int e = GATHER == kGatherMask ? 31 : (int)0x80000000u;
+            if (kk < p.Kr) {
+                const int c = kk / p.RS;
+                const int rs = kk - c * p.RS;
+                const int r = rs / p.S;
+                const int s = rs - r * p.S;
+                const int toff = ((c * p.H + r) * p.W + s) * 4;
+                e = GATHER == kGatherMask ? ((toff << 5) | rs) : toff;
+            }
+            stab[kk] = e;
+        }
+        if (GATHER == kGatherNoPad && m >= p.M) lane_off = (int)0x80000000u;
+    }
+    if constexpr (GATHER == kGatherMask) {
+        if (m < p.M) {
+            inv = 0x80000000u;
+            for (int r = 0; r < p.R; ++r)
+                for (int s = 0; s < p.S; ++s)
+                    if ((unsigned)(hb + r) >= (unsigned)p.H || (unsigned)(wb + s) >= (unsigned)p.W)
+                        inv |= 1u << (r * p.S + s);
+        }
+    }
+    if constexpr (GATHER != kGatherScalar) __syncthreads();
+
+    float xr[KRUN];
+    auto load_x = [&](int kslab) {
+        const int kk0 = kslab + kgrp * KRUN;  // uniform
+        if constexpr (GATHER != kGatherScalar) {
+#pragma unroll
+            for (int j = 0; j < KRUN; j += 4) {
+                const int4 e4 = *reinterpret_cast<const int4*>(&stab[kk0 + j]);
+                const int es[4] = {e4.x, e4.y, e4.z, e4.w};
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    int voff;
+                    if constexpr (GATHER == kGatherMask) {
+                        const unsigned bad = (inv >> (es[u] & 31)) & 1u;
+                        voff = (lane_off + (int)((unsigned)es[u] >> 5)) | (int)(bad << 31);
+                    } else {
+                        voff = (int)((unsigned)lane_off + (unsigned)es[u]);
+                    }
+                    xr[j + u] =
+                        __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, voff, 0, 0));
+                }
+            }
+            return;
+        }
+        int c = kk0 / p.RS;
+        const int rs = kk0 - c * p.RS;
+        int r = rs / p.S;
+        int s = rs - r * p.S;
+        int toff = ((c * p.H + r) * p.W + s) * 4;  // byte offset of tap (c, r, s)
+#pragma unroll
+        for (int j = 0; j < KRUN; ++j) {
+            const bool ok = (kk0 + j < p.Kr) && ((unsigned)(hb + r) < (unsigned)p.H) &&
+                            ((unsigned)(wb + s) < (unsigned)p.W);
+            const int voff = ok ? lane_off + toff : kOutOfRange;
+            xr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, voff, 0, 0));
+            // next tap: s, then r, then c
+            ++s;
+            toff += 4;
+            const bool wrap_s = (s == p.S);
+            s = wrap_s ? 0 : s;
+            r += wrap_s ? 1 : 0;
+            toff += wrap_s ? (p.W - p.S) * 4 : 0;
+            const bool wrap_r = (r == p.R);
+            r = wrap_r ? 0 : r;
+            toff += wrap_r ? (p.HW - p.R * p.W) * 4 : 0;
+        }
+    };
+    auto store_x = [&](int buf) {
+        float* dst = &sB[buf][mloc * LDK + kgrp * KRUN];
+#pragma unroll
+        for (int j = 0; j < KRUN; j += 4)
+            *reinterpret_cast<float4*>(dst + j) = make_float4(xr[j], xr[j + 1], xr[j + 2], xr[j + 3]);
+    };
+
+    // ---- weight tile loads: rows k0.. of the group's [Kg][Kr] block, through a
+    // buffer resource as well (rows past the group or taps past the reduction
+    // read as zero).  Items past the tile land in spare LDS rows never read.
+    const __amdgpu_buffer_rsrc_t wres =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.w), (short)0, p.wbytes, 0x00020000);
+    constexpr int VW = VEC_W ? 4 : 1;
+    int w_off[WV], w_col[WV], w_lds[WV];
+    bool w_rowok[WV];
+#pragma unroll
+    for (int i = 0; i < WV; ++i) {
+        const int idx = tid + i * NT;
+        const int row = idx / (BK / VW);
+        w_col[i] = (idx % (BK / VW)) * VW;
+        w_rowok[i] = row < TM && k0 + row < p.Kg;
+        w_off[i] = w_rowok[i] ? ((g * p.Kg + k0 + row) * p.Kr + w_col[i]) * 4 : 0;
+        w_lds[i] = row * LDK + w_col[i];
+    }
+    float wr[WV * VW];
+    auto load_w = [&](int kslab) {
+#pragma unroll
+        for (int i = 0; i < WV; ++i) {
+            if constexpr (VEC_W) {
+                const bool ok = w_rowok[i] && (kslab + w_col[i] < p.Kr);
+                const int voff = ok ? w_off[i] + kslab * 4 : kOutOfRange;
+                // Cast the whole vector: a bit-cast of one element of an
+                // ext_vector lvalue reads element 0 with this compiler.
+                typedef float f32x4 __attribute__((ext_vector_type(4)));
+                const f32x4 v =
+                    __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(wres, voff, 0, 0));
+                wr[4 * i] = v[0];
+                wr[4 * i + 1] = v[1];
+                wr[4 * i + 2] = v[2];
+                wr[4 * i + 3] = v[3];
+            } else {
+                const bool ok = w_rowok[i] && (kslab + w_col[i] < p.Kr);
+                const int voff = ok ? w_off[i] + kslab * 4 : kOutOfRange;
+                wr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wres, voff, 0, 0));
+            }
+        }
+    };
+    auto store_w = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < WV; ++i) {
+            if constexpr (VEC_W)
+                *reinterpret_cast<float4*>(&sA[buf][w_lds[i]]) =
+                    make_float4(wr[4 * i], wr[4 * i + 1], wr[4 * i + 2], wr[4 * i + 3]);
+            else
+                sA[buf][w_lds[i]] = wr[i];
+        }
+    };
+
+    // ---- matrix-core work of one slab
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WNW;
+    const int wn = wave % WNW;
+    const int half = lane >> 5;
+    const int l32 = lane & 31;
+    floatx16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    auto compute = [&](int buf) {
+        float a[FM][BK / 2];
+        float b[FN][BK / 2];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const float* src = &sA[buf][(wm * FM * 32 + i * 32 + l32) * LDK + half * (BK / 2)];
+#pragma unroll
+            for (int t = 0; t < BK / 2; t += 4) {
+                const float4 v = *reinterpret_cast<const float4*>(src + t);
+                a[i][t] = v.x; a[i][t + 1] = v.y; a[i][t + 2] = v.z; a[i][t + 3] = v.w;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const float* src = &sB[buf][(wn * FN * 32 + j * 32 + l32) * LDK + half * (BK / 2)];
+#pragma unroll
+            for (int t = 0; t < BK / 2; t += 4) {
+                const float4 v = *reinterpret_cast<const float4*>(src + t);
+                b[j][t] = v.x; b[j][t + 1] = v.y; b[j][t + 2] = v.z; b[j][t + 3] = v.w;
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < BK / 2; ++t)
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][t], b[j][t], acc[i][j], 0, 0, 0);
+    };
+
+    // ---- main loop: slab s computes from LDS while slab s+1 loads from memory
+    // The body is one basic block: the last iteration loads a slab past the
+    // reduction (all zeros) into the idle buffer, which nothing reads.  The
+    // scheduling hints spread the next slab's loads and address arithmetic
+    // between the matrix-core instructions of the current slab, so that the
+    // wave keeps issuing while the matrix core works.
+    load_x(0);
+    load_w(0);
+    store_x(0);
+    store_w(0);
+    __syncthreads();
+    for (int sl = 0; sl < nslab; ++sl) {
+        const int cur = sl & 1;
+        load_x((sl + 1) * BK);
+        load_w((sl + 1) * BK);
+        compute(cur);
+        store_x(cur ^ 1);
+        store_w(cur ^ 1);
+        schedule_slab<FM * FN * (BK / 2), (FM + FN) * (BK / 8), KRUN + WV>();
+        __syncthreads();
+    }
+
+    // ---- epilogue: bias, ReLU, NCHW store (lanes = consecutive pixels)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+        const int mc = m0 + wn * FN * 32 + j * 32 + l32;
+        if (mc >= p.M) continue;
+        const int n = mc / p.PQ;
+        const int pq = mc - n * p.PQ;
+        float* yb = p.y + n * p.K * p.PQ + pq;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int kr = k0 + wm * FM * 32 + i * 32 + 8 * (v / 4) + 4 * half + (v % 4);
+                if (kr < p.Kg) {
+                    const int ko = g * p.Kg + kr;
+                    float val = acc[i][j][v];
+                    if (p.bias) val += p.bias[ko];
+                    if (p.relu) val = val > 0.0f ? val : 0.0f;
+                    yb[ko * p.PQ] = val;
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- configurations
+typedef int (*LaunchFn)(const ConvParams&, int G, bool vec_w, hipStream_t st);
+
+template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W, int GATHER>
+inline void launch_kernel(const ConvParams& prm, dim3 grid, dim3 block, size_t shm, hipStream_t st) {
+    hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, VEC_W, GATHER>), grid, block, shm, st, prm);
+}
+
+// Picks the gather mode for the shape and launches one configuration.
+template <int WMW, int WNW, int FM, int FN, int BK>
+int launch_cfg(const ConvParams& prm, int G, bool vec_w, hipStream_t st) {
+    constexpr int TM = WMW * FM * 32;
+    constexpr int TN = WNW * FN * 32;
+    dim3 grid(ceil_div(prm.M, TN), ceil_div(prm.Kg, TM), G);
+    dim3 block(64 * WMW * WNW);
+    // tap tables are at most 32 KiB of LDS
+    const int tab_entries = (ceil_div(prm.Kr, BK) + 1) * BK;
+    const bool tab_fits = tab_entries * 4 <= 32768;
+    int mode = kGatherScalar;
+    if (tab_fits && prm.ph == 0 && prm.pw == 0)
+        mode = kGatherNoPad;
+    else if (tab_fits && prm.RS <= 31 && (int64_t)prm.Cg * prm.HW * 4 < ((int64_t)1 << 27))
+        mode = kGatherMask;
+    const size_t shm = mode == kGatherScalar ? 0 : (size_t)tab_entries * 4;
+    if (vec_w) {
+        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, true, kGatherNoPad>(prm, grid, block, shm, st);
+        else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, true, kGatherMask>(prm, grid, block, shm, st);
+        else launch_kernel<WMW, WNW, FM, FN, BK, true, kGatherScalar>(prm, grid, block, shm, st);
+    } else {
+        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, false, kGatherNoPad>(prm, grid, block, shm, st);
+        else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, false, kGatherMask>(prm, grid, block, shm, st);
+        else launch_kernel<WMW, WNW, FM, FN, BK, false, kGatherScalar>(prm, grid, block, shm, st);
+    }
+    return check_launch("conv2d_igemm_f32");
+}
+
+// The configurations: index, waves along output channels, waves along
+// pixels, 32x32 blocks per wave along channels and pixels, slab length.
+#define CNN_CONV_CONFIGS(X)      \
+    X(0, 2, 2, 2, 2, 16)  /* 128 x 128 */  \
+    X(1, 2, 2, 2, 2, 32)  /* 128 x 128 */  \
+    X(2, 4, 1, 1, 2, 16)  /* 128 x 64 */   \
+    X(3, 4, 1, 1, 2, 32)  /* 128 x 64 */   \
+    X(4, 1, 4, 2, 1, 16)  /* 64 x 128 */   \
+    X(5, 1, 4, 2, 1, 32)  /* 64 x 128 */   \
+    X(6, 1, 4, 3, 1, 16)  /* 96 x 128 */   \
+    X(7, 1, 4, 3, 1, 32)  /* 96 x 128 */   \
+    X(8, 1, 4, 1, 1, 16)  /* 32 x 128 */   \
+    X(9, 2, 2, 1, 1, 16)  /* 64 x 64 */    \
+    X(10, 2, 2, 1, 1, 32) /* 64 x 64 */    \
+    X(11, 2, 4, 2, 2, 16) /* 128 x 256, 8 waves */ \
+    X(12, 1, 2, 3, 2, 16) /* 96 x 128, 2 waves */  \
+    X(13, 2, 1, 2, 2, 16) /* 128 x 64, 2 waves */
+
+#define CNN_CONV_DECLARE(I, WMW, WNW, FM, FN, BK) \
+    int launch_c##I(const ConvParams& prm, int G, bool vec_w, hipStream_t st);
+CNN_CONV_CONFIGS(CNN_CONV_DECLARE)
+
+// Defines launch_c<I> (one translation unit per group of configurations).
+#define CNN_CONV_DEFINE(I, WMW, WNW, FM, FN, BK)                                   \
+    int launch_c##I(const ConvParams& prm, int G, bool vec_w, hipStream_t st) {    \
+        return launch_cfg<WMW, WNW, FM, FN, BK>(prm, G, vec_w, st);                \
+    }
+
+}  // namespace conv
+}  // namespace cnn

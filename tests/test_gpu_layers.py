@@ -275,9 +275,13 @@ def test_binding_errors(gpu):
 # ---------------------------------------------------------------- every tile configuration
 CFG_SHAPES = [
     # N, C, H, W, K, R, S, stride, pad, G
-    # reductions divisible by 4 (128-bit weight loads) and not (32-bit loads)
+    # reductions divisible by 4 (128-bit weight loads) and not (32-bit loads);
+    # gather modes: padded filters of <= 31 taps (mask), unpadded (no-pad),
+    # padded 7x7 and a reduction too long for the LDS tap table (scalar)
     (2, 8, 12, 13, 70, 3, 3, 1, 1, 1),
     (2, 32, 9, 9, 130, 1, 1, 1, 0, 2),
+    (2, 3, 23, 21, 40, 7, 7, 2, 3, 1),
+    (1, 1024, 5, 6, 36, 3, 3, 1, 1, 1),
     (2, 5, 13, 11, 70, 3, 3, 1, 1, 1),
     (3, 6, 17, 19, 130, 5, 5, 2, 2, 2),
     (1, 3, 31, 29, 97, 11, 11, 4, 0, 1),
