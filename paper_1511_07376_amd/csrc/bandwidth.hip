@@ -57,6 +57,89 @@ __global__ void __launch_bounds__(kThreads) maxpool_f32(PoolParams p) {
     }
 }
 
+// Division by a runtime constant through a multiply-high (exact for n < 2^31).
+struct FastDiv {
+    unsigned d, m, l;
+};
+FastDiv make_fastdiv(unsigned d) {
+    unsigned l = 0;
+    while ((1u << l) < d) ++l;
+    const uint64_t m = ((((uint64_t)1 << l) - d) << 32) / d + 1;
+    return FastDiv{d, (unsigned)m, l};
+}
+__device__ inline unsigned fdiv(unsigned n, FastDiv f) { return (__umulhi(f.m, n) + n) >> f.l; }
+
+// Pooling with the input staged in LDS: a workgroup takes a run of whole
+// (n, c) planes, which is one contiguous stretch of memory, reads it with
+// fully coalesced loads into LDS, then computes every output of those planes
+// from LDS and writes them contiguously.  Window size and stride are
+// template constants for the common 3x3/2 and 2x2/2 windows (KH = 0: taken
+// from the parameters).
+constexpr int kPoolLdsBytes = 16 * 1024;  // = kThreads * 16 floats: loaded in one round
+
+template <int MODE, bool WITH_IDX, int KH, int KW, int SH, int SW>  // MODE 0: max, 1: average
+__global__ void __launch_bounds__(kThreads)
+pool_staged_f32(PoolParams p, int planes_per_block, int nplanes, FastDiv fpq, FastDiv fq) {
+    extern __shared__ float tile[];
+    const int kh = KH ? KH : p.kh, kw = KW ? KW : p.kw;
+    const int sh = KH ? SH : p.sh, sw = KW ? SW : p.sw;
+    const int HW = p.H * p.W, PQ = p.P * p.Q;
+    for (int pl0 = blockIdx.x * planes_per_block; pl0 < nplanes; pl0 += gridDim.x * planes_per_block) {
+        const int np = min(planes_per_block, nplanes - pl0);
+        const float* src = p.x + (size_t)pl0 * HW;
+        const int len = np * HW;
+        {  // len <= 16 * kThreads: every load of the run is in flight at once
+            float v[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const int i = threadIdx.x + u * kThreads;
+                v[u] = i < len ? src[i] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const int i = threadIdx.x + u * kThreads;
+                if (i < len) tile[i] = v[u];
+            }
+        }
+        __syncthreads();
+        const int outs = np * PQ;
+        for (int o = threadIdx.x; o < outs; o += kThreads) {
+            const int pl = (int)fdiv(o, fpq);
+            const int r = o - pl * PQ;
+            const int pp = (int)fdiv(r, fq);
+            const int q = r - pp * p.Q;
+            const float* plane = tile + pl * HW;
+            const int hs = pp * sh - p.ph, ws = q * sw - p.pw;
+            const int h0 = max(hs, 0), w0 = max(ws, 0);
+            const int h1 = min(hs + kh, p.H), w1 = min(ws + kw, p.W);
+            float out;
+            if constexpr (MODE == 0) {
+                int bi = h0 * p.W + w0;  // first maximum in row-major order
+                float best = plane[bi];
+                for (int h = h0; h < h1; ++h)
+                    for (int w = w0; w < w1; ++w) {
+                        const float v = plane[h * p.W + w];
+                        if (v > best) {
+                            best = v;
+                            bi = h * p.W + w;
+                        }
+                    }
+                out = best;
+                if (WITH_IDX) p.idx[(size_t)pl0 * PQ + o] = bi;
+            } else {
+                const int count = (min(hs + kh, p.H + p.ph) - hs) * (min(ws + kw, p.W + p.pw) - ws);
+                float sum = 0.0f;
+                for (int h = h0; h < h1; ++h)
+                    for (int w = w0; w < w1; ++w) sum += plane[h * p.W + w];
+                out = sum / (float)count;
+            }
+            if (p.relu) out = out > 0.0f ? out : 0.0f;
+            p.y[(size_t)pl0 * PQ + o] = out;
+        }
+        __syncthreads();
+    }
+}
+
 __global__ void __launch_bounds__(kThreads) avgpool_f32(PoolParams p) {
     for (int o = blockIdx.x * kThreads + threadIdx.x; o < p.total; o += gridDim.x * kThreads) {
         const int q = o % p.Q;
@@ -187,6 +270,34 @@ int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y
     p.total = s.N * s.C * s.P * s.Q;
     p.relu = relu;
     if (p.total == 0) return CNN_OK;
+    const int plane_bytes = s.H * s.W * 4;
+    if (plane_bytes <= kPoolLdsBytes) {
+        const int ppb = kPoolLdsBytes / plane_bytes;
+        const int nplanes = s.N * s.C;
+        const dim3 g(std::min(ceil_div(nplanes, ppb), 1 << 20)), b(kThreads);
+        const size_t shm = (size_t)ppb * plane_bytes;
+        const FastDiv fpq = make_fastdiv(s.P * s.Q), fq = make_fastdiv(s.Q);
+        const bool w33 = s.kh == 3 && s.kw == 3 && s.sh == 2 && s.sw == 2;
+        const bool w22 = s.kh == 2 && s.kw == 2 && s.sh == 2 && s.sw == 2;
+#define CNN_POOL_LAUNCH(M, I)                                                                              \
+    do {                                                                                                   \
+        if (w33)                                                                                           \
+            hipLaunchKernelGGL((pool_staged_f32<M, I, 3, 3, 2, 2>), g, b, shm, st, p, ppb, nplanes, fpq, fq); \
+        else if (w22)                                                                                      \
+            hipLaunchKernelGGL((pool_staged_f32<M, I, 2, 2, 2, 2>), g, b, shm, st, p, ppb, nplanes, fpq, fq); \
+        else                                                                                               \
+            hipLaunchKernelGGL((pool_staged_f32<M, I, 0, 0, 0, 0>), g, b, shm, st, p, ppb, nplanes, fpq, fq); \
+    } while (0)
+        if (mode == CNN_POOL_MAX && idx)
+            CNN_POOL_LAUNCH(0, true);
+        else if (mode == CNN_POOL_MAX)
+            CNN_POOL_LAUNCH(0, false);
+        else
+            CNN_POOL_LAUNCH(1, false);
+#undef CNN_POOL_LAUNCH
+        return check_launch("pool_staged_f32");
+    }
+    // planes larger than the staging buffer: one thread per output from memory
     const dim3 grid(grid_for(p.total)), block(kThreads);
     if (mode == CNN_POOL_MAX) {
         if (idx)

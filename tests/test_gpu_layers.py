@@ -179,6 +179,9 @@ POOL_CASES = [
     (1, 5, 9, 9, "max", (3, 2), (2, 3), (1, 0), True), (1, 5, 9, 9, "avg", (3, 2), (2, 3), (1, 0), False),
     (3, 2, 7, 9, "max", 4, 3, 2, False), (3, 2, 7, 9, "avg", 4, 3, 2, False),
     (1, 1, 1, 1, "max", 1, 1, 0, False), (2, 4, 5, 5, "avg", 5, 1, 0, False),
+    # planes of more than 48 KiB (pooled straight from memory, not staged in LDS)
+    (1, 2, 130, 120, "max", 3, 2, 1, False), (1, 2, 130, 120, "avg", 3, 2, 1, True),
+    (3, 5, 57, 57, "max", 3, 3, 0, False),
 ]
 
 
