@@ -138,6 +138,9 @@ FC_CASES = [
     (256, 9216, 4096, True, [0, 100, 255]), (256, 4096, 4096, True, [1, 254]),
     (1, 37, 3, False, None), (5, 1001, 31, True, None), (33, 129, 129, False, None),
     (65, 260, 7, True, None), (130, 64, 300, False, None), (3, 4, 1, True, None),
+    # k-streaming kernel (batches up to 64, inputs a multiple of 4): 1 to 4 row
+    # blocks of 16, with and without the reduction split over workgroups
+    (48, 512, 300, True, None), (20, 3072, 4100, True, [0, 7, 19]), (64, 96, 17, False, None),
 ]
 
 

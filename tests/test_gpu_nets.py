@@ -119,3 +119,32 @@ def test_net_output_canary_and_workspace_reuse(gpu):
         assert np.all(out[batch * 10:] == -777.0)
         assert_gemm_close(out[: batch * 10].reshape(batch, 10),
                           oracle.net_fwd(net, x, wl.make_params(net, 5)), 500, f"lenet B{batch}")
+
+
+@pytest.mark.parametrize("C,H,mode,k,s,p,relu", [
+    (96, 55, "max", 3, 2, 0, False),    # AlexNet layers 2-3 shape
+    (40, 27, "max", 3, 2, 1, True),     # channel count not a multiple of 32, padding, ReLU
+    (7, 13, "avg", 3, 2, 0, False),
+    (33, 9, "max", 2, 2, 0, False),
+    (5, 120, "max", 3, 2, 0, False),
+])
+def test_lrn_then_pool_matches_separate_layers(gpu, C, H, mode, k, s, p, relu):
+    """An LRN followed by pooling in a network gives values and indices equal,
+    bit for bit, to those of the two single-layer calls."""
+    print(f"lrn+pool C{C} H{H} {mode} k{k} s{s} p{p} relu{int(relu)}", flush=True)
+    net = wl.Net("lrn_pool", (C, H, H), (wl.lrn(5, 1e-2, 0.75, 2.0),
+                                        wl.pool(mode, k, s, p, relu=relu)),
+                 weight_std=0.0, bias_std=0.0, input_dist="normal")
+    x = wl.make_input(net, 3, 8) * 4
+    model = gpu.Network(net, wl.make_params(net, 8), pool_index=(mode == "max"))
+    xd = to_dev(x)
+    y = to_host(model(xd))
+    l = gpu.cnn_lrn_fwd(xd, 5, 1e-2, 0.75, 2.0)
+    r = gpu.cnn_pool_fwd(l, mode, k, s, p, True, relu, with_index=(mode == "max"))
+    if mode == "max":
+        np.testing.assert_array_equal(y, to_host(r[0]))
+        np.testing.assert_array_equal(to_host(model.indices[1]), to_host(r[1]))
+    else:
+        np.testing.assert_array_equal(y, to_host(r))
+    ref = oracle.pool_fwd(oracle.lrn_fwd(x, 5, 1e-2, 0.75, 2.0), mode, (k, k), (s, s), (p, p), True, relu)
+    np.testing.assert_allclose(y, ref, rtol=2e-5, atol=1e-6 * np.abs(x).max())
