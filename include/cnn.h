@@ -63,8 +63,12 @@ int cnn_pool_out_shape(int H, int W, int kh, int kw, int sh, int sw,
  *   x    [N][C][H][W]      w [K][C/G][R][S]      bias [K] or NULL
  *   y    [N][K][P][Q]      (P, Q from cnn_conv2d_out_shape)
  * groups must divide C and K.  fuse_relu = 1 applies y = max(y, 0) in the
- * same kernel (a Conv+ReLU layer).  Errors: CNN_ERR_INVALID for null x/w/y,
- * non-positive sizes or bad shapes. */
+ * same kernel (a Conv+ReLU layer).  When the output has too few tiles to
+ * occupy the GPU (small batches), the reduction is split across workgroups:
+ * y is first set to the bias, the partial sums are added with fp32 atomics
+ * and the ReLU runs as a separate pass; the summation order, and so the last
+ * bits of y, may then differ from call to call.  Errors: CNN_ERR_INVALID for
+ * null x/w/y, non-positive sizes or bad shapes. */
 int cnn_conv2d_fwd(const float* x, int N, int C, int H, int W,
                    const float* w, int K, int R, int S, const float* bias,
                    int sh, int sw, int ph, int pw, int groups, int fuse_relu,

@@ -18,6 +18,7 @@ int check_launch(const char* what);
 inline hipStream_t as_stream(cnn_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
 
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Largest element count a tensor may have (offsets inside kernels are int32).
 constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;

@@ -15,9 +15,9 @@ struct ConvConfig {
     LaunchFn launch;
 };
 
-#define CNN_CONV_ENTRY(I, WMW, WNW, FM, FN, BK)                                            \
-    ConvConfig{#WMW "x" #WNW " waves, " #FM "x" #FN " blocks, BK " #BK, WMW * FM * 32, WNW * FN * 32, \
-               BK, 64 * WMW * WNW, &launch_c##I},
+#define CNN_CONV_ENTRY(I, WMW, WNW, FM, FN, BK, KS)                                        \
+    ConvConfig{#WMW "x" #WNW " waves, " #FM "x" #FN " blocks, BK " #BK ", " #KS " slab groups",      \
+               WMW * FM * 32, WNW * FN * 32, BK, 64 * WMW * WNW * KS, &launch_c##I},
 
 const ConvConfig kConfigs[] = {CNN_CONV_CONFIGS(CNN_CONV_ENTRY)};
 constexpr int kNumConfigs = sizeof(kConfigs) / sizeof(kConfigs[0]);
@@ -34,6 +34,27 @@ int heuristic_config(const ConvParams& p, int G) {
     return blocks >= 512 ? 0 : 2;
 }
 
+// Reduction chunks for a configuration: when its output tiles would leave
+// more than half of the 256 compute units idle, split the reduction so that
+// about 512 workgroups run, keeping at least 8 slabs per chunk.
+void choose_splits(ConvParams& p, const ConvConfig& c) {
+    const int tiles = ceil_div(p.M, c.tn) * ceil_div(p.Kg, c.tm) * p.G;
+    const int nslab = ceil_div(p.Kr, c.bk);
+    int splits = 1;
+    if (tiles <= 128) splits = std::max(1, std::min(ceil_div(512, tiles), nslab / 8));
+    const int slabs_per_chunk = ceil_div(nslab, splits);
+    p.kchunk = splits > 1 ? slabs_per_chunk * c.bk : p.Kr;
+    p.splits = splits > 1 ? ceil_div(p.Kr, p.kchunk) : 1;
+}
+
+// y[n][k][pq] = bias[k] (or 0): the starting value of a split reduction.
+__global__ void conv_fill_bias(float* __restrict__ y, const float* __restrict__ bias, int K, int PQ,
+                               int64_t total) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x)
+        y[i] = bias ? bias[(i / PQ) % K] : 0.0f;
+}
+
 }  // namespace
 }  // namespace conv
 
@@ -41,6 +62,7 @@ using conv::ConvParams;
 using conv::kConfigs;
 using conv::kNumConfigs;
 using conv::heuristic_config;
+using conv::choose_splits;
 
 int conv2d_num_configs() { return kNumConfigs; }
 
@@ -61,6 +83,9 @@ int launch_conv2d(const ConvShape& s, const float* x, const float* w, const floa
     prm.HW = s.H * s.W;
     prm.PQ = s.P * s.Q;
     prm.relu = relu;
+    prm.G = s.G;
+    prm.splits = 1;
+    prm.kchunk = prm.Kr;
     if (s.N == 0) return CNN_OK;
     const bool vec_w = (prm.Kr % 4 == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
     const int64_t wbytes = (int64_t)s.K * prm.Kr * 4;
@@ -77,15 +102,27 @@ int launch_conv2d(const ConvShape& s, const float* x, const float* w, const floa
         cfg = heuristic_config(prm, s.G);
     }
     if (cfg >= kNumConfigs) return fail(CNN_ERR_UNSUPPORTED, "conv: no configuration %d", cfg);
+    // One split decision for every launch of the call (the last one may hold
+    // fewer images: splitting it the same way is still correct).
+    prm.M = per_launch * prm.PQ;
+    choose_splits(prm, kConfigs[cfg]);
+    const int64_t total = (int64_t)s.N * s.K * prm.PQ;
+    if (prm.splits > 1) {
+        hipLaunchKernelGGL(conv::conv_fill_bias, dim3((unsigned)std::min<int64_t>(ceil_div64(total, 256), 4096)),
+                           dim3(256), 0, st, y, bias, s.K, prm.PQ, total);
+        const int rc = check_launch("conv_fill_bias");
+        if (rc != CNN_OK) return rc;
+    }
     for (int n0 = 0; n0 < s.N; n0 += per_launch) {
         const int nb = std::min(per_launch, s.N - n0);
         prm.x = x + (size_t)n0 * img;
         prm.y = y + (size_t)n0 * s.K * prm.PQ;
         prm.M = nb * prm.PQ;
         prm.xbytes = (int)(nb * img * 4);
-        const int rc = kConfigs[cfg].launch(prm, s.G, vec_w, st);
+        const int rc = kConfigs[cfg].launch(prm, vec_w, st);
         if (rc != CNN_OK) return rc;
     }
+    if (prm.splits > 1 && relu) return launch_relu(y, y, total, st);
     return CNN_OK;
 }
 

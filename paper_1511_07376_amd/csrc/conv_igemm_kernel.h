@@ -27,6 +27,12 @@
 // slab and lanes 32-63 the last BK/2 (an MFMA step consumes one tap per lane
 // half), so each lane reads BK/2 consecutive LDS words per fragment with
 // 128-bit loads.  The order of a sum changes its value only by rounding.
+//
+// Split reduction: when the output has too few tiles to occupy the chip (a
+// batch of one image, say), grid z also splits the reduction into chunks of
+// kchunk taps; each workgroup then adds its partial tile into an output that
+// holds the bias already, with fp32 atomics, and a ReLU, if any, runs after
+// the last chunk.
 #pragma once
 
 #include <cstdlib>
@@ -52,6 +58,9 @@ struct ConvParams {
     int xbytes;  // bytes of x covered by this launch (< 2^31)
     int wbytes;  // bytes of w (< 2^31)
     int relu;
+    int G;       // groups (grid z = G * splits)
+    int splits;  // reduction chunks; > 1: partial tiles are added atomically
+    int kchunk;  // taps per chunk (a multiple of every slab length; Kr if splits == 1)
 };
 
 // Instruction-scheduling pattern of one slab (LLVM sched_group_barrier masks:
@@ -86,12 +95,18 @@ __device__ inline void schedule_slab() {
 //    out-of-range pixels start at 2^31: an element costs one add.
 constexpr int kGatherScalar = 0, kGatherMask = 1, kGatherNoPad = 2;
 
-template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W, int GATHER>
-__global__ void __launch_bounds__(64 * WMW * WNW)
+// KS > 1: the workgroup holds KS groups of WMW x WNW waves that reduce
+// interleaved slabs (group g takes slabs g, g + KS, ...) into the same
+// output tile; their partial tiles are summed through LDS before the
+// epilogue.  This gives small-pixel-count layers more waves without
+// shrinking each wave's tile.
+template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W, int GATHER, int KS>
+__global__ void __launch_bounds__(64 * WMW * WNW * KS)
 conv2d_igemm_f32(ConvParams p) {
     constexpr int TM = WMW * FM * 32;  // output channels per workgroup
     constexpr int TN = WNW * FN * 32;  // output pixels per workgroup
-    constexpr int NT = 64 * WMW * WNW;
+    constexpr int NT = 64 * WMW * WNW;  // threads per slab group
+    constexpr int NTB = NT * KS;        // threads per workgroup
     constexpr int LDK = BK + 4;        // padded LDS row (conflict-free 128-bit reads)
     constexpr int KGROUPS = NT / TN;   // threads sharing one pixel column of the gather
     constexpr int KRUN = BK / KGROUPS; // consecutive taps gathered per thread
@@ -102,11 +117,19 @@ conv2d_igemm_f32(ConvParams p) {
     constexpr int WV = (WTOT + NT - 1) / NT;                // ... per thread
     constexpr int AROWS = WV * NT / (VEC_W ? BK / 4 : BK);  // TM rows + spare rows
 
-    __shared__ __attribute__((aligned(16))) float sA[2][AROWS * LDK];  // weights  [k][kk]
-    __shared__ __attribute__((aligned(16))) float sB[2][TN * LDK];  // im2col   [m][kk]
+    // LDS: [buffer][group] weight tiles [k][kk], then [buffer][group] im2col
+    // tiles [m][kk]; reused at the end for the groups' partial tiles
+    constexpr int A_ELEMS = AROWS * LDK, B_ELEMS = TN * LDK;
+    __shared__ __attribute__((aligned(16))) float smem[2 * KS * (A_ELEMS + B_ELEMS)];
+    static_assert((KS - 1) * TM * TN <= 2 * KS * (A_ELEMS + B_ELEMS), "reduction space");
 
-    const int tid = threadIdx.x;
-    const int g = blockIdx.z;
+    const int tid = threadIdx.x % NT;                                   // thread within its group
+    const int sgrp = KS > 1 ? __builtin_amdgcn_readfirstlane(threadIdx.x / NT) : 0;  // slab group
+    auto sA = [&](int buf) { return smem + (buf * KS + sgrp) * A_ELEMS; };
+    auto sB = [&](int buf) { return smem + 2 * KS * A_ELEMS + (buf * KS + sgrp) * B_ELEMS; };
+    const int g = blockIdx.z % p.G;
+    const int kbeg = (blockIdx.z / p.G) * p.kchunk;  // first tap of this chunk
+    const int klen = min(p.kchunk, p.Kr - kbeg);      // taps in this chunk
     const int m0 = blockIdx.x * TN;
     const int k0 = blockIdx.y * TM;
 
@@ -131,15 +154,16 @@ conv2d_igemm_f32(ConvParams p) {
     const __amdgpu_buffer_rsrc_t xres =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.x), (short)0, p.xbytes, 0x00020000);
 
-    const int nslab = (p.Kr + BK - 1) / BK;
-    extern __shared__ __attribute__((aligned(16))) int stab[];  // (nslab + 1) * BK entries
+    const int nslab = (klen + BK - 1) / BK;
+    const int niter = (nslab + KS - 1) / KS;  // slabs per group
+    extern __shared__ __attribute__((aligned(16))) int stab[];  // (niter + 1) * KS * BK entries
     unsigned inv = 0xffffffffu;
     if constexpr (GATHER != kGatherScalar) {
-        for (int kk = tid; kk < (nslab + 1) * BK; kk += NT) {
+        for (int kk = threadIdx.x; kk < (niter + 1) * KS * BK; kk += NTB) {
             int e = GATHER == kGatherMask ? 31 : (int)0x80000000u;
-            if (kk < p.Kr) {
-                const int c = kk / p.RS;
-                const int rs = kk - c * p.RS;
+            if (kk < klen) {
+                const int c = (kbeg + kk) / p.RS;
+                const int rs = kbeg + kk - c * p.RS;
                 const int r = rs / p.S;
                 const int s = rs - r * p.S;
                 const int toff = ((c * p.H + r) * p.W + s) * 4;
@@ -183,14 +207,15 @@ conv2d_igemm_f32(ConvParams p) {
             }
             return;
         }
-        int c = kk0 / p.RS;
-        const int rs = kk0 - c * p.RS;
+        const int ka0 = kbeg + kk0;  // absolute tap index
+        int c = ka0 / p.RS;
+        const int rs = ka0 - c * p.RS;
         int r = rs / p.S;
         int s = rs - r * p.S;
         int toff = ((c * p.H + r) * p.W + s) * 4;  // byte offset of tap (c, r, s)
 #pragma unroll
         for (int j = 0; j < KRUN; ++j) {
-            const bool ok = (kk0 + j < p.Kr) && ((unsigned)(hb + r) < (unsigned)p.H) &&
+            const bool ok = (kk0 + j < klen) && ((unsigned)(hb + r) < (unsigned)p.H) &&
                             ((unsigned)(wb + s) < (unsigned)p.W);
             const int voff = ok ? lane_off + toff : kOutOfRange;
             xr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, voff, 0, 0));
@@ -207,7 +232,7 @@ conv2d_igemm_f32(ConvParams p) {
         }
     };
     auto store_x = [&](int buf) {
-        float* dst = &sB[buf][mloc * LDK + kgrp * KRUN];
+        float* dst = sB(buf) + mloc * LDK + kgrp * KRUN;
 #pragma unroll
         for (int j = 0; j < KRUN; j += 4)
             *reinterpret_cast<float4*>(dst + j) = make_float4(xr[j], xr[j + 1], xr[j + 2], xr[j + 3]);
@@ -227,7 +252,7 @@ conv2d_igemm_f32(ConvParams p) {
         const int row = idx / (BK / VW);
         w_col[i] = (idx % (BK / VW)) * VW;
         w_rowok[i] = row < TM && k0 + row < p.Kg;
-        w_off[i] = w_rowok[i] ? ((g * p.Kg + k0 + row) * p.Kr + w_col[i]) * 4 : 0;
+        w_off[i] = w_rowok[i] ? ((g * p.Kg + k0 + row) * p.Kr + kbeg + w_col[i]) * 4 : 0;
         w_lds[i] = row * LDK + w_col[i];
     }
     float wr[WV * VW];
@@ -235,7 +260,7 @@ conv2d_igemm_f32(ConvParams p) {
 #pragma unroll
         for (int i = 0; i < WV; ++i) {
             if constexpr (VEC_W) {
-                const bool ok = w_rowok[i] && (kslab + w_col[i] < p.Kr);
+                const bool ok = w_rowok[i] && (kslab + w_col[i] < klen);
                 const int voff = ok ? w_off[i] + kslab * 4 : kOutOfRange;
                 // Cast the whole vector: a bit-cast of one element of an
                 // ext_vector lvalue reads element 0 with this compiler.
@@ -247,7 +272,7 @@ conv2d_igemm_f32(ConvParams p) {
                 wr[4 * i + 2] = v[2];
                 wr[4 * i + 3] = v[3];
             } else {
-                const bool ok = w_rowok[i] && (kslab + w_col[i] < p.Kr);
+                const bool ok = w_rowok[i] && (kslab + w_col[i] < klen);
                 const int voff = ok ? w_off[i] + kslab * 4 : kOutOfRange;
                 wr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wres, voff, 0, 0));
             }
@@ -257,10 +282,10 @@ conv2d_igemm_f32(ConvParams p) {
 #pragma unroll
         for (int i = 0; i < WV; ++i) {
             if constexpr (VEC_W)
-                *reinterpret_cast<float4*>(&sA[buf][w_lds[i]]) =
+                *reinterpret_cast<float4*>(sA(buf) + w_lds[i]) =
                     make_float4(wr[4 * i], wr[4 * i + 1], wr[4 * i + 2], wr[4 * i + 3]);
             else
-                sA[buf][w_lds[i]] = wr[i];
+                sA(buf)[w_lds[i]] = wr[i];
         }
     };
 
@@ -284,7 +309,7 @@ conv2d_igemm_f32(ConvParams p) {
         float b[FN][BK / 2];
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
-            const float* src = &sA[buf][(wm * FM * 32 + i * 32 + l32) * LDK + half * (BK / 2)];
+            const float* src = sA(buf) + (wm * FM * 32 + i * 32 + l32) * LDK + half * (BK / 2);
 #pragma unroll
             for (int t = 0; t < BK / 2; t += 4) {
                 const float4 v = *reinterpret_cast<const float4*>(src + t);
@@ -293,7 +318,7 @@ conv2d_igemm_f32(ConvParams p) {
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-            const float* src = &sB[buf][(wn * FN * 32 + j * 32 + l32) * LDK + half * (BK / 2)];
+            const float* src = sB(buf) + (wn * FN * 32 + j * 32 + l32) * LDK + half * (BK / 2);
 #pragma unroll
             for (int t = 0; t < BK / 2; t += 4) {
                 const float4 v = *reinterpret_cast<const float4*>(src + t);
@@ -315,20 +340,45 @@ conv2d_igemm_f32(ConvParams p) {
     // scheduling hints spread the next slab's loads and address arithmetic
     // between the matrix-core instructions of the current slab, so that the
     // wave keeps issuing while the matrix core works.
-    load_x(0);
-    load_w(0);
+    load_x(sgrp * BK);
+    load_w(sgrp * BK);
     store_x(0);
     store_w(0);
     __syncthreads();
-    for (int sl = 0; sl < nslab; ++sl) {
-        const int cur = sl & 1;
-        load_x((sl + 1) * BK);
-        load_w((sl + 1) * BK);
+    for (int it = 0; it < niter; ++it) {
+        const int cur = it & 1;
+        load_x(((it + 1) * KS + sgrp) * BK);
+        load_w(((it + 1) * KS + sgrp) * BK);
         compute(cur);
         store_x(cur ^ 1);
         store_w(cur ^ 1);
         schedule_slab<FM * FN * (BK / 2), (FM + FN) * (BK / 8), KRUN + WV>();
         __syncthreads();
+    }
+
+    // ---- sum the slab groups' partial tiles (lanes on consecutive words)
+    if constexpr (KS > 1) {
+        constexpr int E = FM * FN * 16;
+        if (sgrp > 0) {
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v)
+                        smem[((sgrp - 1) * E + (i * FN + j) * 16 + v) * NT + tid] = acc[i][j][v];
+        }
+        __syncthreads();
+        if (sgrp > 0) return;
+#pragma unroll
+        for (int q = 1; q < KS; ++q)
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v)
+                        acc[i][j][v] += smem[((q - 1) * E + (i * FN + j) * 16 + v) * NT + tid];
     }
 
     // ---- epilogue: bias, ReLU, NCHW store (lanes = consecutive pixels)
@@ -347,9 +397,13 @@ conv2d_igemm_f32(ConvParams p) {
                 if (kr < p.Kg) {
                     const int ko = g * p.Kg + kr;
                     float val = acc[i][j][v];
-                    if (p.bias) val += p.bias[ko];
-                    if (p.relu) val = val > 0.0f ? val : 0.0f;
-                    yb[ko * p.PQ] = val;
+                    if (p.splits > 1) {
+                        atomicAdd(yb + ko * p.PQ, val);
+                    } else {
+                        if (p.bias) val += p.bias[ko];
+                        if (p.relu) val = val > 0.0f ? val : 0.0f;
+                        yb[ko * p.PQ] = val;
+                    }
                 }
             }
         }
@@ -357,22 +411,22 @@ conv2d_igemm_f32(ConvParams p) {
 }
 
 // ---------------------------------------------------------------- configurations
-typedef int (*LaunchFn)(const ConvParams&, int G, bool vec_w, hipStream_t st);
+typedef int (*LaunchFn)(const ConvParams&, bool vec_w, hipStream_t st);
 
-template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W, int GATHER>
+template <int WMW, int WNW, int FM, int FN, int BK, int KS, bool VEC_W, int GATHER>
 inline void launch_kernel(const ConvParams& prm, dim3 grid, dim3 block, size_t shm, hipStream_t st) {
-    hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, VEC_W, GATHER>), grid, block, shm, st, prm);
+    hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, VEC_W, GATHER, KS>), grid, block, shm, st, prm);
 }
 
 // Picks the gather mode for the shape and launches one configuration.
-template <int WMW, int WNW, int FM, int FN, int BK>
-int launch_cfg(const ConvParams& prm, int G, bool vec_w, hipStream_t st) {
+template <int WMW, int WNW, int FM, int FN, int BK, int KS>
+int launch_cfg(const ConvParams& prm, bool vec_w, hipStream_t st) {
     constexpr int TM = WMW * FM * 32;
     constexpr int TN = WNW * FN * 32;
-    dim3 grid(ceil_div(prm.M, TN), ceil_div(prm.Kg, TM), G);
-    dim3 block(64 * WMW * WNW);
+    dim3 grid(ceil_div(prm.M, TN), ceil_div(prm.Kg, TM), prm.G * prm.splits);
+    dim3 block(64 * WMW * WNW * KS);
     // tap tables are at most 32 KiB of LDS
-    const int tab_entries = (ceil_div(prm.Kr, BK) + 1) * BK;
+    const int tab_entries = (ceil_div(ceil_div(prm.kchunk, BK), KS) + 1) * KS * BK;
     const bool tab_fits = tab_entries * 4 <= 32768;
     int mode = kGatherScalar;
     if (tab_fits && prm.ph == 0 && prm.pw == 0)
@@ -381,43 +435,46 @@ int launch_cfg(const ConvParams& prm, int G, bool vec_w, hipStream_t st) {
         mode = kGatherMask;
     const size_t shm = mode == kGatherScalar ? 0 : (size_t)tab_entries * 4;
     if (vec_w) {
-        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, true, kGatherNoPad>(prm, grid, block, shm, st);
-        else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, true, kGatherMask>(prm, grid, block, shm, st);
-        else launch_kernel<WMW, WNW, FM, FN, BK, true, kGatherScalar>(prm, grid, block, shm, st);
+        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, true, kGatherNoPad>(prm, grid, block, shm, st);
+        else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, true, kGatherMask>(prm, grid, block, shm, st);
+        else launch_kernel<WMW, WNW, FM, FN, BK, KS, true, kGatherScalar>(prm, grid, block, shm, st);
     } else {
-        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, false, kGatherNoPad>(prm, grid, block, shm, st);
-        else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, false, kGatherMask>(prm, grid, block, shm, st);
-        else launch_kernel<WMW, WNW, FM, FN, BK, false, kGatherScalar>(prm, grid, block, shm, st);
+        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, false, kGatherNoPad>(prm, grid, block, shm, st);
+        else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, false, kGatherMask>(prm, grid, block, shm, st);
+        else launch_kernel<WMW, WNW, FM, FN, BK, KS, false, kGatherScalar>(prm, grid, block, shm, st);
     }
     return check_launch("conv2d_igemm_f32");
 }
 
 // The configurations: index, waves along output channels, waves along
-// pixels, 32x32 blocks per wave along channels and pixels, slab length.
+// pixels, 32x32 blocks per wave along channels and pixels, slab length,
+// slab groups per workgroup.
 #define CNN_CONV_CONFIGS(X)      \
-    X(0, 2, 2, 2, 2, 16)  /* 128 x 128 */  \
-    X(1, 2, 2, 2, 2, 32)  /* 128 x 128 */  \
-    X(2, 4, 1, 1, 2, 16)  /* 128 x 64 */   \
-    X(3, 4, 1, 1, 2, 32)  /* 128 x 64 */   \
-    X(4, 1, 4, 2, 1, 16)  /* 64 x 128 */   \
-    X(5, 1, 4, 2, 1, 32)  /* 64 x 128 */   \
-    X(6, 1, 4, 3, 1, 16)  /* 96 x 128 */   \
-    X(7, 1, 4, 3, 1, 32)  /* 96 x 128 */   \
-    X(8, 1, 4, 1, 1, 16)  /* 32 x 128 */   \
-    X(9, 2, 2, 1, 1, 16)  /* 64 x 64 */    \
-    X(10, 2, 2, 1, 1, 32) /* 64 x 64 */    \
-    X(11, 2, 4, 2, 2, 16) /* 128 x 256, 8 waves */ \
-    X(12, 1, 2, 3, 2, 16) /* 96 x 128, 2 waves */  \
-    X(13, 2, 1, 2, 2, 16) /* 128 x 64, 2 waves */
+    X(0, 2, 2, 2, 2, 16, 1)  /* 128 x 128 */  \
+    X(1, 2, 2, 2, 2, 32, 1)  /* 128 x 128 */  \
+    X(2, 4, 1, 1, 2, 16, 1)  /* 128 x 64 */   \
+    X(3, 4, 1, 1, 2, 32, 1)  /* 128 x 64 */   \
+    X(4, 1, 4, 2, 1, 16, 1)  /* 64 x 128 */   \
+    X(5, 1, 4, 2, 1, 32, 1)  /* 64 x 128 */   \
+    X(6, 1, 4, 3, 1, 16, 1)  /* 96 x 128 */   \
+    X(7, 1, 4, 3, 1, 32, 1)  /* 96 x 128 */   \
+    X(8, 1, 4, 1, 1, 16, 1)  /* 32 x 128 */   \
+    X(9, 2, 2, 1, 1, 16, 1)  /* 64 x 64 */    \
+    X(10, 2, 2, 1, 1, 32, 1) /* 64 x 64 */    \
+    X(11, 2, 4, 2, 2, 16, 1) /* 128 x 256, 8 waves */ \
+    X(12, 1, 2, 3, 2, 16, 1) /* 96 x 128, 2 waves */  \
+    X(13, 2, 1, 2, 2, 16, 1) /* 128 x 64, 2 waves */  \
+    X(14, 2, 2, 1, 1, 16, 2) /* 64 x 64, 2 slab groups of 4 waves */  \
+    X(15, 2, 1, 2, 2, 16, 2) /* 128 x 64, 2 slab groups of 2 waves */
 
-#define CNN_CONV_DECLARE(I, WMW, WNW, FM, FN, BK) \
-    int launch_c##I(const ConvParams& prm, int G, bool vec_w, hipStream_t st);
+#define CNN_CONV_DECLARE(I, WMW, WNW, FM, FN, BK, KS) \
+    int launch_c##I(const ConvParams& prm, bool vec_w, hipStream_t st);
 CNN_CONV_CONFIGS(CNN_CONV_DECLARE)
 
 // Defines launch_c<I> (one translation unit per group of configurations).
-#define CNN_CONV_DEFINE(I, WMW, WNW, FM, FN, BK)                                   \
-    int launch_c##I(const ConvParams& prm, int G, bool vec_w, hipStream_t st) {    \
-        return launch_cfg<WMW, WNW, FM, FN, BK>(prm, G, vec_w, st);                \
+#define CNN_CONV_DEFINE(I, WMW, WNW, FM, FN, BK, KS)                               \
+    int launch_c##I(const ConvParams& prm, bool vec_w, hipStream_t st) {           \
+        return launch_cfg<WMW, WNW, FM, FN, BK, KS>(prm, vec_w, st);               \
     }
 
 }  // namespace conv

@@ -291,6 +291,13 @@ CFG_SHAPES = [
     (2, 5, 13, 11, 70, 3, 3, 1, 1, 1),
     (3, 6, 17, 19, 130, 5, 5, 2, 2, 2),
     (1, 3, 31, 29, 97, 11, 11, 4, 0, 1),
+    # few output tiles: the reduction is split across workgroups (mask, no-pad
+    # and scalar gathers; chunks that start inside a filter; a ragged last
+    # chunk with 32-bit weight loads and two groups)
+    (1, 256, 7, 7, 64, 3, 3, 1, 1, 1),
+    (1, 512, 6, 5, 40, 1, 1, 1, 0, 1),
+    (1, 64, 9, 9, 20, 7, 7, 1, 3, 1),
+    (1, 100, 5, 5, 30, 3, 3, 1, 1, 2),
 ]
 
 
@@ -329,3 +336,25 @@ def test_autotune_records_and_reuses(gpu):
     y = gpu.cnn_conv2d_fwd(to_dev(x), to_dev(w), None, st, pd, G, False)   # uses the record
     assert_gemm_close(to_host(y), ref, C * R * S, "tuned record")
     gpu.cnn_tuning_clear()
+
+
+@pytest.mark.parametrize("bias,relu", [(False, False), (True, False), (False, True)])
+def test_conv_split_reduction_bias_relu_and_bounds(gpu, bias, relu):
+    """A batch of one image with a long reduction takes the split path (output
+    pre-filled with the bias, partial tiles added atomically, ReLU after):
+    every combination of bias and ReLU matches, and nothing past the output
+    is written."""
+    N, C, H, W, K = 1, 384, 6, 6, 50
+    x = wl.normal((N, C, H, W), 1.0, 21, 0)
+    w = wl.normal((K, C, 3, 3), 1.0, 21, 1)
+    b = wl.normal((K,), 1.0, 21, 2) if bias else None
+    n = N * K * H * W
+    for cfg in (-1, 2, 9, 14):
+        print(f"split conv config {cfg} bias{int(bias)} relu{int(relu)}", flush=True)
+        buf = torch.full((n + 4096,), -321.0, device="cuda")
+        gpu.cnn_conv2d_fwd(to_dev(x), to_dev(w), to_dev(b) if bias else None, 1, 1, 1, relu,
+                           y=buf[:n].view(N, K, H, W), config=cfg)
+        out = to_host(buf)
+        assert np.all(out[n:] == -321.0)
+        ref = oracle.conv2d_fwd(x, w, b, (1, 1), (1, 1), 1, relu)
+        assert_gemm_close(out[:n].reshape(N, K, H, W), ref, C * 9, f"split config {cfg}")
