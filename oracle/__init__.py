@@ -43,10 +43,12 @@ def _load():
     lib.oracle_pool_fwd.argtypes = [_fp] + [_c_int] * 13 + [_fp, _ip]
     lib.oracle_lrn_fwd.argtypes = [_fp] + [_c_int] * 5 + [ctypes.c_float] * 3 + [_fp]
     lib.oracle_relu_fwd.argtypes = [_fp, _fp, ctypes.c_int64]
+    lib.oracle_softmax_fwd.argtypes = [_fp, _c_int, _c_int, _c_int, _fp]
     lib.oracle_set_threads.argtypes = [_c_int]
     lib.oracle_get_threads.restype = _c_int
     for name in ("oracle_conv2d_out_shape", "oracle_pool_out_shape", "oracle_conv2d_fwd",
-                 "oracle_fc_fwd", "oracle_pool_fwd", "oracle_lrn_fwd", "oracle_relu_fwd"):
+                 "oracle_fc_fwd", "oracle_pool_fwd", "oracle_lrn_fwd", "oracle_relu_fwd",
+                 "oracle_softmax_fwd"):
         getattr(lib, name).restype = _c_int
     _lib = lib
     return lib
@@ -163,6 +165,18 @@ def relu_fwd(x) -> np.ndarray:
     return y
 
 
+def softmax_fwd(x) -> np.ndarray:
+    """Softmax across axis 1 of an [N][C] or [N][C][H][W] array."""
+    x = _f32(x)
+    if x.ndim < 2:
+        raise ValueError("oracle: softmax needs an [N][C...] array")
+    N, C = x.shape[0], x.shape[1]
+    HW = int(np.prod(x.shape[2:])) if x.ndim > 2 else 1
+    y = np.empty_like(x)
+    _check(_load().oracle_softmax_fwd(_ptr(x), N, C, HW, _ptr(y)), "softmax_fwd")
+    return y
+
+
 def net_fwd(net, x, params, keep: bool = False, pool_index: bool = False):
     """Run a ``workloads.Net`` on input x with ``workloads.make_params`` params.
 
@@ -197,6 +211,8 @@ def net_fwd(net, x, params, keep: bool = False, pool_index: bool = False):
             a = lrn_fwd(a, layer.size, layer.alpha, layer.beta, layer.k)
         elif layer.kind == "relu":
             a = relu_fwd(a)
+        elif layer.kind == "softmax":
+            a = softmax_fwd(a)
         else:
             raise ValueError(f"oracle: unknown layer kind {layer.kind}")
         if layer.relu and layer.kind != "relu":

@@ -212,3 +212,30 @@ int oracle_relu_fwd(const float* x, float* y, int64_t n) {
     for (int64_t i = 0; i < n; ++i) y[i] = relu_f(x[i]);
     return 0;
 }
+
+/* Softmax across channels (Sec. 3.1 lists the layer; the definition is the
+ * usual normalized exponential, over axis 1 as in Caffe): for every image n
+ * and position i of the H*W plane,
+ *   y[n,c,i] = exp(x[n,c,i]) / sum_{c'} exp(x[n,c',i]).
+ * Both exponentials are taken of x - max_c' x[n,c',i], which leaves the
+ * quotient unchanged and keeps exp from overflowing; everything in double,
+ * rounded once. */
+int oracle_softmax_fwd(const float* x, int N, int C, int HW, float* y) {
+    if (N < 0 || C <= 0 || HW <= 0) return -1;
+    if (N > 0 && (!x || !y)) return -1;
+    int64_t cols = (int64_t)N * HW;
+#pragma omp parallel for schedule(static)
+    for (int64_t col = 0; col < cols; ++col) {
+        const int64_t n = col / HW, i = col % HW;
+        const int64_t cs = HW;  /* distance between channels */
+        const float* xc = x + n * (int64_t)C * HW + i;
+        float* yc = y + n * (int64_t)C * HW + i;
+        double m = xc[0];
+        for (int c = 1; c < C; ++c)
+            if (xc[c * cs] > m) m = xc[c * cs];
+        double sum = 0.0;
+        for (int c = 0; c < C; ++c) sum += exp((double)xc[c * cs] - m);
+        for (int c = 0; c < C; ++c) yc[c * cs] = (float)(exp((double)xc[c * cs] - m) / sum);
+    }
+    return 0;
+}

@@ -73,6 +73,12 @@ int oracle_lrn_fwd(const float* x, int N, int C, int H, int W, int size,
 /* y[i] = x[i] > 0 ? x[i] : +0.0f */
 int oracle_relu_fwd(const float* x, float* y, int64_t n);
 
+/* Softmax across channels of x viewed as [N][C][HW] (HW = H*W; 1 after a
+ * fully connected layer):
+ *   y[n,c,i] = exp(x[n,c,i] - m) / sum_{c'} exp(x[n,c',i] - m),
+ *   m = max_{c'} x[n,c',i]. */
+int oracle_softmax_fwd(const float* x, int N, int C, int HW, float* y);
+
 /* OpenMP threads used by the loops above (default: all). */
 void oracle_set_threads(int n);
 int oracle_get_threads(void);

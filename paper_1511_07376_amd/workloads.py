@@ -26,7 +26,7 @@ from typing import Dict, List, Optional, Tuple
 import numpy as np
 
 __all__ = [
-    "Layer", "Net", "conv", "fc", "pool", "lrn", "relu",
+    "Layer", "Net", "conv", "fc", "pool", "lrn", "relu", "softmax",
     "NETS", "lenet", "cifar_quick", "alexnet",
     "SWEEP_SHAPES", "SWEEP_BATCHES",
     "rng_for", "uniform01", "normal", "make_input", "make_params",
@@ -38,7 +38,7 @@ __all__ = [
 class Layer:
     """One layer of a network description.
 
-    kind: "conv", "fc", "pool", "lrn" or "relu".
+    kind: "conv", "fc", "pool", "lrn", "relu" or "softmax" (across channels).
     conv: in_channels, out_channels, kernel (R, S), stride, pad, groups, relu.
     fc:   in_features, out_features, relu.
     pool: mode ("max" or "avg"), kernel, stride, pad, ceil, relu (applied
@@ -109,6 +109,10 @@ def lrn(size: int = 5, alpha: float = 1e-4, beta: float = 0.75, k: float = 1.0) 
 
 def relu() -> Layer:
     return Layer("relu")
+
+
+def softmax() -> Layer:
+    return Layer("softmax")
 
 
 @dataclass(frozen=True)

@@ -14,6 +14,7 @@ import pytest
 import oracle
 import test_oracle_conv_fc as tc
 import test_oracle_pool_lrn_net as tp
+import test_oracle_softmax as ts
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
 
@@ -44,6 +45,10 @@ MUTANTS = [
     ("lrn beta sign", "pow(scale, -(double)beta)", "pow(scale, (double)beta)"),
     ("relu keeps negative zero", "return v > 0.0f ? v : 0.0f;", "return v >= 0.0f ? v : 0.0f;"),
     ("conv floor rounds up", "*P = (H + 2 * ph - R) / sh + 1;", "*P = (H + 2 * ph - R + sh - 1) / sh + 1;"),
+    ("softmax without the max shift", "double m = xc[0];", "double m = 0.0;"),
+    ("softmax not normalized", "- m) / sum);", "- m));"),
+    ("softmax sum skips a channel", "for (int c = 0; c < C; ++c) sum +=", "for (int c = 1; c < C; ++c) sum +="),
+    ("softmax over the wrong axis", "const int64_t cs = HW;", "const int64_t cs = 1;"),
 ]
 
 
@@ -69,6 +74,10 @@ def _pins():
         ("lrn torch", lambda: tp.test_lrn_matches_torch(7, 5, 1e-4, 0.75, 1.0)),
         ("lrn torch 2", lambda: tp.test_lrn_matches_torch(16, 5, 0.5, 0.75, 2.0)),
         ("relu", tp.test_relu_definition),
+        ("softmax logistic", lambda: ts.test_softmax_two_classes_is_logistic(1.0, -2.0)),
+        ("softmax overflow", ts.test_softmax_large_inputs_do_not_overflow),
+        ("softmax sums", ts.test_softmax_rows_sum_to_one_and_keep_order),
+        ("softmax axis", lambda: ts.test_softmax_channel_axis_matches_torch((2, 3, 2, 2))),
     ]
 
 
