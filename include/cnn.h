@@ -16,7 +16,7 @@
  *    enqueued on `stream` (a hipStream_t; NULL = the null stream) and the
  *    caller synchronises.
  *  - Input and output buffers must not overlap, except that cnn_relu_fwd
- *    allows y == x.  A pointer to a tensor with no elements (batch N = 0,
+ *    and cnn_softmax_fwd allow y == x.  A pointer to a tensor with no elements (batch N = 0,
  *    length n = 0) may be NULL; such a call validates and enqueues nothing.
  *  - No exception or abort crosses the ABI.  cnn_last_error() returns a
  *    thread-local message describing the last non-OK status of this thread.
@@ -155,6 +155,14 @@ int cnn_lrn_fwd(const float* x, int N, int C, int H, int W, int size,
  * y == x (in place) is allowed. */
 int cnn_relu_fwd(const float* x, float* y, int64_t n, cnn_stream_t stream);
 
+/* Softmax layer (Sec. 3.1), across channels of x viewed as [N][C][HW]
+ * (HW = H*W of an NCHW tensor, 1 after a fully connected layer):
+ *   y[n,c,i] = exp(x[n,c,i] - m) / sum_{c'} exp(x[n,c',i] - m),
+ *   m = max_{c'} x[n,c',i].
+ * y == x (in place) is allowed; other overlaps are CNN_ERR_INVALID.  Inputs
+ * must be finite (NaN / infinity give unspecified results). */
+int cnn_softmax_fwd(const float* x, int N, int C, int HW, float* y, cnn_stream_t stream);
+
 /* ---------------------------------------------------------------- networks
  * A network is an array of layer descriptors executed in order (the paper's
  * NetFile layer list, Sec. 3.2, and compute(), Sec. 3.3).  Parameters are
@@ -165,7 +173,8 @@ typedef enum cnn_layer_type {
     CNN_LAYER_FC = 1,
     CNN_LAYER_POOL = 2,
     CNN_LAYER_LRN = 3,
-    CNN_LAYER_RELU = 4
+    CNN_LAYER_RELU = 4,
+    CNN_LAYER_SOFTMAX = 5
 } cnn_layer_type;
 
 typedef struct cnn_layer_desc {
@@ -206,8 +215,9 @@ size_t cnn_net_workspace_bytes(const cnn_layer_desc* layers, int n_layers,
 /* Runs the network on x [N][C][H][W] and writes the last layer's output to y
  * ([N][outC][outH][outW]).  ws is caller-owned device memory of at least
  * cnn_net_workspace_bytes(); intermediates live there.  A RELU layer that
- * follows a CONV, FC or POOL layer is executed inside that layer (Sec. 3.5).
- * Every layer is validated before the first launch. */
+ * follows a CONV, FC or POOL layer is executed inside that layer (Sec. 3.5);
+ * other RELU layers and SOFTMAX layers run in place.  A SOFTMAX layer uses
+ * only the type field.  Every layer is validated before the first launch. */
 int cnn_net_fwd(const cnn_layer_desc* layers, int n_layers, const float* x,
                 int N, int C, int H, int W, float* y, void* ws, size_t ws_bytes,
                 cnn_stream_t stream);

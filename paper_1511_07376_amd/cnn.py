@@ -31,6 +31,7 @@ _ip = ctypes.POINTER(ctypes.c_int)
 CNN_OK, CNN_ERR_INVALID, CNN_ERR_UNSUPPORTED, CNN_ERR_HIP, CNN_ERR_WORKSPACE = 0, -1, -2, -3, -4
 CNN_POOL_MAX, CNN_POOL_AVG = 0, 1
 CNN_LAYER_CONV, CNN_LAYER_FC, CNN_LAYER_POOL, CNN_LAYER_LRN, CNN_LAYER_RELU = 0, 1, 2, 3, 4
+CNN_LAYER_SOFTMAX = 5
 
 
 class cnn_layer_desc(ctypes.Structure):
@@ -56,6 +57,7 @@ lib.cnn_pool_fwd.argtypes = [_p, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i,
 lib.cnn_lrn_fwd.argtypes = [_p, _i, _i, _i, _i, _i, ctypes.c_float, ctypes.c_float, ctypes.c_float,
                             _p, _p]
 lib.cnn_relu_fwd.argtypes = [_p, _p, ctypes.c_int64, _p]
+lib.cnn_softmax_fwd.argtypes = [_p, _i, _i, _i, _p, _p]
 _descp = ctypes.POINTER(cnn_layer_desc)
 lib.cnn_net_out_shape.argtypes = [_descp, _i, _i, _i, _i, _i, _ip, _ip, _ip]
 lib.cnn_net_workspace_bytes.argtypes = [_descp, _i, _i, _i, _i, _i]
@@ -75,13 +77,14 @@ lib.cnn_tuning_clear.argtypes = []
 lib.cnn_last_error.restype = ctypes.c_char_p
 lib.cnn_version.restype = ctypes.c_char_p
 for _name in ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
-              "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_net_out_shape", "cnn_net_fwd",
+              "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_softmax_fwd", "cnn_net_out_shape",
+              "cnn_net_fwd",
               "cnn_net_fwd_timed", "cnn_conv2d_fwd_config", "cnn_conv2d_num_configs",
               "cnn_set_autotune", "cnn_tuning_import", "cnn_tuning_clear"):
     getattr(lib, _name).restype = _i
 
 EXPORTED = ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
-            "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_net_out_shape",
+            "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_softmax_fwd", "cnn_net_out_shape",
             "cnn_net_workspace_bytes", "cnn_net_fwd", "cnn_net_fwd_timed", "cnn_last_error",
             "cnn_version", "cnn_conv2d_num_configs", "cnn_conv2d_config_name",
             "cnn_conv2d_fwd_config", "cnn_set_autotune", "cnn_tuning_export",
@@ -250,6 +253,23 @@ def cnn_relu_fwd(x, y=None, stream=None):
     return y
 
 
+def cnn_softmax_fwd(x, y=None, stream=None):
+    """Softmax across dim 1 of an [N][C] or [N][C][H][W] tensor; pass y=x for
+    in place."""
+    if x.dim() < 2:
+        raise ValueError("softmax: x must be [N][C...]")
+    if y is None:
+        y = torch.empty_like(x)
+    if y.numel() != x.numel():
+        raise ValueError("softmax: x and y differ in size")
+    N, C = x.shape[0], x.shape[1]
+    HW = 1
+    for d in x.shape[2:]:
+        HW *= d
+    _ok(lib.cnn_softmax_fwd(_dev(x, "x"), N, C, HW, _dev(y, "y"), _stream(stream)))
+    return y
+
+
 # ---------------------------------------------------------------- networks
 class Network:
     """A layer-descriptor array bound to device-resident parameters.
@@ -303,6 +323,8 @@ class Network:
                 d.lrn_alpha, d.lrn_beta, d.lrn_k = layer.alpha, layer.beta, layer.k
             elif layer.kind == "relu":
                 d.type = CNN_LAYER_RELU
+            elif layer.kind == "softmax":
+                d.type = CNN_LAYER_SOFTMAX
             else:
                 raise ValueError(f"unknown layer kind {layer.kind}")
             d.weight = w.data_ptr() if w is not None else None
@@ -315,7 +337,7 @@ class Network:
         oc, oh, ow = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
         _ok(lib.cnn_net_out_shape(self.descs, len(self.descs), N, C, H, W, ctypes.byref(oc),
                                   ctypes.byref(oh), ctypes.byref(ow)))
-        last = [l for l in self.net.layers if l.kind != "relu"]
+        last = [l for l in self.net.layers if l.kind not in ("relu", "softmax")]
         if last and last[-1].kind == "fc":
             return (N, oc.value)
         return (N, oc.value, oh.value, ow.value)

@@ -116,6 +116,12 @@ int check_lrn(int N, int C, int H, int W, int size) {
     return CNN_OK;
 }
 
+int check_softmax(int N, int C, int HW) {
+    if (N < 0 || C <= 0 || HW <= 0) return fail(CNN_ERR_INVALID, "softmax: N=%d C=%d HW=%d", N, C, HW);
+    if (too_big(N, C, HW)) return fail(CNN_ERR_UNSUPPORTED, "softmax: tensor exceeds 2^31-1 elements");
+    return CNN_OK;
+}
+
 int check_fc(int N, int I, int O) {
     if (N < 0 || I <= 0 || O <= 0) return fail(CNN_ERR_INVALID, "fc: N=%d I=%d O=%d", N, I, O);
     if (too_big(N, I) || too_big(N, O) || too_big(O, I))
@@ -189,6 +195,10 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
                 rc = check_lrn(N, c, h, w, d.lrn_size);
                 if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
                 break;
+            case CNN_LAYER_SOFTMAX:
+                rc = check_softmax(N, c, h * w);
+                if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
+                break;
             case CNN_LAYER_RELU:
                 // Embedded into the preceding conv / FC / pooling layer (Sec. 3.5).
                 if (prev_exec >= 0 && (plan[prev_exec].type == CNN_LAYER_CONV ||
@@ -249,8 +259,9 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
         if (p.skipped) continue;
         const cnn_layer_desc& d = L[i];
         float* out = (i == last) ? y : buf[next_buf];
-        // an in-place ReLU keeps its buffer
-        if (p.type == CNN_LAYER_RELU && i != last && cur != x) out = const_cast<float*>(cur);
+        // an in-place ReLU or softmax keeps its buffer
+        if ((p.type == CNN_LAYER_RELU || p.type == CNN_LAYER_SOFTMAX) && i != last && cur != x)
+            out = const_cast<float*>(cur);
         switch (p.type) {
             case CNN_LAYER_CONV:
                 rc = conv2d_dispatch(p.conv, cur, d.weight, d.bias, p.relu, out, st);
@@ -267,6 +278,9 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
                 break;
             case CNN_LAYER_RELU:
                 rc = launch_relu(cur, out, (int64_t)N * p.inC * p.inH * p.inW, st);
+                break;
+            case CNN_LAYER_SOFTMAX:
+                rc = launch_softmax(cur, N, p.inC, p.inH * p.inW, out, st);
                 break;
         }
         if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
@@ -351,6 +365,20 @@ int cnn_relu_fwd(const float* x, float* y, int64_t n, cnn_stream_t stream) {
     if (n != 0 && (!x || !y)) return fail(CNN_ERR_INVALID, "relu: null x or y");
     if (n < 0) return fail(CNN_ERR_INVALID, "relu: negative length");
     return launch_relu(x, y, n, as_stream(stream));
+}
+
+int cnn_softmax_fwd(const float* x, int N, int C, int HW, float* y, cnn_stream_t stream) {
+    if (N != 0 && (!x || !y)) return fail(CNN_ERR_INVALID, "softmax: null x or y");
+    int rc = check_softmax(N, C, HW);
+    if (rc) return rc;
+    if (x != y) {
+        const size_t bytes = (size_t)N * C * HW * sizeof(float);
+        const char* xb = reinterpret_cast<const char*>(x);
+        const char* yb = reinterpret_cast<const char*>(y);
+        if (xb < yb + bytes && yb < xb + bytes)
+            return fail(CNN_ERR_INVALID, "softmax: x and y overlap without being equal");
+    }
+    return launch_softmax(x, N, C, HW, y, as_stream(stream));
 }
 
 int cnn_net_out_shape(const cnn_layer_desc* layers, int n_layers, int N, int C, int H, int W,

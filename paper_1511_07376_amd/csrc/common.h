@@ -55,5 +55,6 @@ int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y
 int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha, float beta,
                float k, float* y, hipStream_t st);
 int launch_relu(const float* x, float* y, int64_t n, hipStream_t st);
+int launch_softmax(const float* x, int N, int C, int HW, float* y, hipStream_t st);
 
 }  // namespace cnn

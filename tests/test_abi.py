@@ -109,6 +109,8 @@ def _descs(net):
         elif layer.kind == "lrn":
             d.type, d.lrn_size = cnn.CNN_LAYER_LRN, layer.size
             d.lrn_alpha, d.lrn_beta, d.lrn_k = layer.alpha, layer.beta, layer.k
+        elif layer.kind == "softmax":
+            d.type = cnn.CNN_LAYER_SOFTMAX
         else:
             d.type = cnn.CNN_LAYER_RELU
     return descs
@@ -146,6 +148,32 @@ def test_fc_pool_lrn_relu_reject():
     assert L.cnn_lrn_fwd(FAKE, 1, 4, 4, 4, 0, 1e-4, 0.75, 1.0, FAKE, 0) == cnn.CNN_ERR_INVALID
     assert L.cnn_relu_fwd(FAKE, FAKE, -1, 0) == cnn.CNN_ERR_INVALID
     assert L.cnn_relu_fwd(0, FAKE, 4, 0) == cnn.CNN_ERR_INVALID
+
+
+def test_softmax_rejects():
+    assert L.cnn_softmax_fwd(FAKE, -1, 10, 1, FAKE, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_softmax_fwd(FAKE, 2, 0, 1, FAKE, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_softmax_fwd(FAKE, 2, 10, 0, FAKE, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_softmax_fwd(0, 2, 10, 1, FAKE, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_softmax_fwd(FAKE, 70000, 1000, 100, FAKE, 0) == cnn.CNN_ERR_UNSUPPORTED
+    # partial overlap (y four floats past x) is refused; N = 0 enqueues nothing
+    assert L.cnn_softmax_fwd(FAKE, 2, 10, 1, FAKE + 16, 0) == cnn.CNN_ERR_INVALID
+    assert "overlap" in cnn.cnn_last_error()
+    assert L.cnn_softmax_fwd(0, 0, 10, 1, 0, 0) == cnn.CNN_OK
+
+
+def test_net_with_softmax_layers_out_shape():
+    """Softmax keeps the shape: after FC [N][O], after a conv [N][C][H][W]."""
+    net = wl.Net("sm", (3, 12, 12), (wl.conv(3, 6, 3), wl.softmax(), wl.pool("max", 2, 2),
+                                     wl.fc(6 * 5 * 5, 7), wl.softmax()), 0.1, 0.1)
+    descs = _descs(net)
+    oc, oh, ow = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    assert L.cnn_net_out_shape(descs, len(descs), 4, 3, 12, 12, ctypes.byref(oc), ctypes.byref(oh),
+                               ctypes.byref(ow)) == 0, cnn.cnn_last_error()
+    assert (oc.value, oh.value, ow.value) == (7, 1, 1)
+    assert L.cnn_net_out_shape(descs, 2, 4, 3, 12, 12, ctypes.byref(oc), ctypes.byref(oh),
+                               ctypes.byref(ow)) == 0
+    assert (oc.value, oh.value, ow.value) == (6, 10, 10)
 
 
 def test_net_rejects_before_launch():

@@ -358,3 +358,42 @@ def test_conv_split_reduction_bias_relu_and_bounds(gpu, bias, relu):
         assert np.all(out[n:] == -321.0)
         ref = oracle.conv2d_fwd(x, w, b, (1, 1), (1, 1), 1, relu)
         assert_gemm_close(out[:n].reshape(N, K, H, W), ref, C * 9, f"split config {cfg}")
+
+
+# ---------------------------------------------------------------- softmax
+def _softmax_rtol(x, hw):
+    """Per-element relative error bound of the GPU softmax against the double
+    oracle: the shifted argument x - m rounded once (|x - m| ulps of 2^-24 in
+    the exponential), exp itself (1 ulp), the sum of C terms (C/64 serial adds
+    per lane plus 6 tree levels across the wave for HW = 1; C serial adds per
+    thread otherwise) and one division; doubled as margin."""
+    C = x.shape[1]
+    span = float(np.max(np.max(x, axis=1, keepdims=True) - x)) if x.size else 0.0
+    adds = C / 64 + 6 if hw == 1 else C
+    return 2 * (span + adds + 2) * 2.0 ** -24
+
+
+@pytest.mark.parametrize("shape", [(1, 1), (3, 10), (64, 1000), (2, 63), (2, 64), (2, 65), (5, 4097),
+                                   (257, 7), (2, 3, 5, 7), (1, 21, 13, 13), (3, 1, 4, 4), (2, 1000, 1, 3)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_softmax(gpu, shape):
+    print(f"softmax {shape}", flush=True)
+    x = wl.normal(shape, 3.0, 22, 0)
+    ref = oracle.softmax_fwd(x)
+    y = to_host(gpu.cnn_softmax_fwd(to_dev(x)))
+    hw = int(np.prod(shape[2:])) if len(shape) > 2 else 1
+    np.testing.assert_allclose(y, ref, rtol=_softmax_rtol(x, hw), atol=1e-37)
+
+
+def test_softmax_in_place_large_values_and_empty(gpu):
+    x = np.array([[1000.0, 999.0, 998.0, -1000.0], [5.0, 5.0, 5.0, 5.0], [88.0, -88.0, 0.0, 1.0]],
+                 dtype=np.float32)
+    xd = to_dev(x)
+    gpu.cnn_softmax_fwd(xd, y=xd)
+    np.testing.assert_allclose(to_host(xd), oracle.softmax_fwd(x), rtol=_softmax_rtol(x, 1), atol=1e-37)
+    assert np.all(to_host(xd)[1] == np.float32(0.25))
+    x4 = wl.normal((2, 5, 3, 3), 2.0, 23, 0)
+    xd = to_dev(x4)
+    gpu.cnn_softmax_fwd(xd, y=xd)
+    np.testing.assert_allclose(to_host(xd), oracle.softmax_fwd(x4), rtol=_softmax_rtol(x4, 9), atol=1e-37)
+    assert gpu.cnn_softmax_fwd(torch.empty((0, 10), device="cuda")).shape == (0, 10)

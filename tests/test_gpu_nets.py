@@ -148,3 +148,25 @@ def test_lrn_then_pool_matches_separate_layers(gpu, C, H, mode, k, s, p, relu):
         np.testing.assert_array_equal(y, to_host(r))
     ref = oracle.pool_fwd(oracle.lrn_fwd(x, 5, 1e-2, 0.75, 2.0), mode, (k, k), (s, s), (p, p), True, relu)
     np.testing.assert_allclose(y, ref, rtol=2e-5, atol=1e-6 * np.abs(x).max())
+
+
+def test_nets_with_softmax(gpu):
+    """LeNet with a softmax after its last FC (one row per image) and a small
+    net with a softmax across the channels of a conv output, mid-network."""
+    lenet_sm = wl.Net("lenet_softmax", wl.lenet.input_chw, wl.lenet.layers + (wl.softmax(),),
+                      wl.lenet.weight_std, 1.0, input_dist="normal")
+    mid = wl.Net("conv_softmax", (3, 16, 16), (
+        wl.conv(3, 12, 3, pad=1, relu=True), wl.softmax(), wl.pool("max", 2, 2),
+        wl.conv(12, 8, 3), wl.softmax(), wl.fc(8 * 6 * 6, 10), wl.softmax(),
+    ), 0.3, 0.1, input_dist="normal")
+    for net, batch in ((lenet_sm, 16), (mid, 5)):
+        print(f"net {net.name} batch {batch}", flush=True)
+        x = wl.make_input(net, batch, 9)
+        params = wl.make_params(net, 9)
+        y = to_host(gpu.Network(net, params)(to_dev(x)))
+        ref = oracle.net_fwd(net, x, params)
+        assert y.shape == ref.shape
+        # a logit error e changes a probability by a factor exp(e): the FC
+        # criterion on the logits becomes a relative one on the output
+        np.testing.assert_allclose(y, ref, rtol=1e-4, atol=1e-30)
+        np.testing.assert_allclose(y.astype(np.float64).sum(axis=1), 1.0, rtol=1e-5)
