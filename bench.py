@@ -62,6 +62,8 @@ def layer_work(net, batch, cnn):
             h, w = p, q
         elif layer.kind == "lrn":
             out.append((name, "lrn", 0, 8 * batch * c * h * w))
+        elif layer.kind == "softmax":
+            out.append((name, "softmax", 0, 8 * batch * c * h * w))
         else:
             out.append((name, "relu", 0, 8 * batch * c * h * w))
     return out
@@ -104,10 +106,17 @@ def cpu_baseline(net, x, params, budget_s):
         oracle.net_fwd(net, x[1:1 + n_more], params)
         t2 = time.perf_counter() - t0
     n = 1 + n_more
+    # the paper's sequential baseline: one thread, one image
+    oracle.set_threads(1)
+    t0 = time.perf_counter()
+    oracle.net_fwd(net, x[:1], params)
+    t_one = time.perf_counter() - t0
+    oracle.set_threads(threads)
     return {"value": n / (t1 + t2), "unit": "images/s", "cores": threads, "kind": "oracle",
             "sample": f"{n} of the {x.shape[0]} images of the same batch through the oracle's "
                       f"layer-by-layer network (double accumulation, OpenMP over images x "
-                      f"channels), {t1 + t2:.1f} s"}
+                      f"channels), {t1 + t2:.1f} s",
+            "value_1_thread": round(1.0 / t_one, 3)}
 
 
 def main():
@@ -126,7 +135,8 @@ def main():
                     help="import this conv tuning table before warm-up (no tuning runs for its shapes)")
     ap.add_argument("--save-tuning", default=None, help="write the tuning table here afterwards")
     ap.add_argument("--graph", action="store_true",
-                    help="also time the steps as replays of a captured HIP graph")
+                    help="time the steps as launches of the network captured as a HIP graph "
+                         "(the library's graph execution mode)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -179,19 +189,19 @@ def main():
 
     graph = None
     if args.graph:
-        # one forward pass captured as a HIP graph and replayed per step
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            model(xd, y=yd)
-        graph.replay()
+        # the library's graph execution mode: one forward pass captured by
+        # cnn_net_graph_create, one graph launch per step
+        graph = cnn.Network(net, params, execution_mode="graph")
+        graph(xd, y=yd)                # eager pass + capture
+        graph(xd, y=yd)
         torch.cuda.synchronize()
 
-    # timed region: K steps of cnn_net_fwd (graph replays with --graph)
+    # timed region: K steps of cnn_net_fwd (graph launches with --graph)
     torch.cuda.synchronize()
     start.record()
     for k in range(args.steps):
         if graph is not None:
-            graph.replay()
+            graph(xd, y=yd)
         else:
             model(xd, y=yd)
     end.record()
@@ -211,6 +221,7 @@ def main():
 
     layer_ms = [float(np.mean([events[k][i].elapsed_time(events[k][i + 1]) for k in range(args.steps)]))
                 for i in range(nl)]
+    step_ms_events = [events[k][0].elapsed_time(events[k][nl]) for k in range(args.steps)]
     work = layer_work(net, batch, cnn)
     layers = []
     for (name, kind, flops, byts), ms in zip(work, layer_ms):
@@ -264,6 +275,7 @@ def main():
         "conv_frac_fp32_mfma_peak": round(conv_tf / PEAK_FP32_MFMA_TFLOPS, 4),
         "conv_ms": round(conv_ms, 5),
         "ms_per_step_with_layer_events": round(ms_step_events, 4),
+        "ms_per_step_with_layer_events_median": round(float(np.median(step_ms_events)), 4),
         "graph_replay": bool(graph is not None),
         "autotune": bool(args.autotune),
         "conv_configs": {" ".join(l.split()[:-1]): cnn.cnn_conv2d_config_name(int(l.split()[-1]))

@@ -203,7 +203,8 @@ typedef struct cnn_layer_desc {
 
 /* Output shape of the network for an N x C x H x W input (outC x outH x outW
  * per image; FC layers give outH = outW = 1).  CNN_ERR_INVALID /
- * CNN_ERR_UNSUPPORTED describe the first bad layer. */
+ * CNN_ERR_UNSUPPORTED describe the first bad layer.  Weight pointers are not
+ * needed here (nor by cnn_net_workspace_bytes). */
 int cnn_net_out_shape(const cnn_layer_desc* layers, int n_layers, int N, int C,
                       int H, int W, int* outC, int* outH, int* outW);
 
@@ -230,6 +231,74 @@ int cnn_net_fwd(const cnn_layer_desc* layers, int n_layers, const float* x,
 int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x,
                       int N, int C, int H, int W, float* y, void* ws,
                       size_t ws_bytes, void* const* events, cnn_stream_t stream);
+
+/* ---------------------------------------------------------------- execution
+ * The paper's engine runs a network either sequentially or in parallel, as
+ * the NetFile's execution_mode says (Sec. 3.5).  Here every layer runs on the
+ * GPU; the two modes are how the layers reach it: PARALLEL enqueues one
+ * network pass per cnn_net_fwd call, GRAPH captures that sequence once into a
+ * HIP graph bound to fixed buffers and replays it (one launch per pass).
+ */
+typedef enum cnn_exec_mode {
+    CNN_EXEC_PARALLEL = 0,
+    CNN_EXEC_GRAPH = 1
+} cnn_exec_mode;
+
+typedef struct cnn_net_graph cnn_net_graph; /* opaque */
+
+/* Captures one cnn_net_fwd(layers, ..., x, y, ws) into a HIP graph; nothing
+ * runs.  The graph holds the pointers given here (x, y, ws, the layers'
+ * weights, biases and index outputs) and the convolution configurations in
+ * force now: a shape that the auto-tuner has not timed yet uses the built-in
+ * heuristic, so run the network once with auto-tuning on before capturing to
+ * replay tuned configurations.  The layer array itself may be freed after
+ * the call.  Returns CNN_OK and *graph, or an error status (validation as in
+ * cnn_net_fwd) with *graph = NULL.  Creating a graph allocates host memory and
+ * a capture stream; it is not meant for the per-image path. */
+int cnn_net_graph_create(const cnn_layer_desc* layers, int n_layers, const float* x,
+                         int N, int C, int H, int W, float* y, void* ws,
+                         size_t ws_bytes, cnn_net_graph** graph);
+
+/* Enqueues one replay of the graph on `stream` (asynchronous, as cnn_net_fwd). */
+int cnn_net_graph_launch(cnn_net_graph* graph, cnn_stream_t stream);
+
+/* Frees the graph (NULL is a no-op).  Replays already enqueued complete. */
+int cnn_net_graph_destroy(cnn_net_graph* graph);
+
+/* ---------------------------------------------------------------- NetFile
+ * A text description of a network and of the engine's parameters (the
+ * paper's NetFile, Sec. 3.2).  One statement per line; '#' starts a comment;
+ * "key value" and "key: value" are both accepted for the parameters:
+ *   input C H W                     input image shape
+ *   execution_mode parallel|graph   (default parallel; "sequential" is
+ *                                   CNN_ERR_UNSUPPORTED: no CPU path here)
+ *   auto_tuning on|off              (default off)
+ *   allocated_ram MIB               parsed and reported only: parameters
+ *                                   stay resident in device memory
+ * and layer statements, in network order:
+ *   conv out=K kernel=R[xS] [stride=..] [pad=..] [groups=G] [in=C] [relu]
+ *   fc out=O [in=I] [relu]
+ *   pool max|avg kernel=K[xK] [stride=..] [pad=..] [ceil=0|1] [relu]
+ *   lrn [size=5] [alpha=1e-4] [beta=0.75] [k=1]
+ *   relu
+ *   softmax
+ * Pairs are "7" or "7x5" (height x width); strides default to 1, pads to 0,
+ * ceil to 1 (the pooling rule of cnn_pool_out_shape), groups to 1.  "relu"
+ * as an option fuses a ReLU after the layer. */
+typedef struct cnn_netfile_config {
+    int32_t in_channels, in_height, in_width; /* from "input"; 0 if absent */
+    int32_t execution_mode;                    /* cnn_exec_mode */
+    int32_t auto_tuning;                       /* 0 or 1 */
+    int32_t allocated_ram_mib;                 /* 0 if absent */
+} cnn_netfile_config;
+
+/* Parses a NUL-terminated NetFile.  With layers == NULL only counts: sets
+ * *n_layers and *config.  Otherwise writes up to max_layers descriptors
+ * (weight, bias and pool_index NULL: the caller sets them) and fails with
+ * CNN_ERR_INVALID if there are more.  Errors name the line; on error the
+ * outputs are unspecified.  Host only, no GPU call. */
+int cnn_netfile_parse(const char* text, cnn_layer_desc* layers, int max_layers,
+                      int* n_layers, cnn_netfile_config* config);
 
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char* cnn_last_error(void);

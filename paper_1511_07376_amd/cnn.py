@@ -11,9 +11,12 @@ from __future__ import annotations
 
 import ctypes
 import os
-from typing import List, Optional, Sequence, Tuple
+from dataclasses import dataclass
+from typing import Dict, List, Optional, Sequence, Tuple
 
 import torch
+
+from . import workloads as _wl
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libcnn.so")
@@ -58,6 +61,15 @@ lib.cnn_lrn_fwd.argtypes = [_p, _i, _i, _i, _i, _i, ctypes.c_float, ctypes.c_flo
                             _p, _p]
 lib.cnn_relu_fwd.argtypes = [_p, _p, ctypes.c_int64, _p]
 lib.cnn_softmax_fwd.argtypes = [_p, _i, _i, _i, _p, _p]
+
+
+class cnn_netfile_config(ctypes.Structure):
+    _fields_ = [("in_channels", ctypes.c_int32), ("in_height", ctypes.c_int32),
+                ("in_width", ctypes.c_int32), ("execution_mode", ctypes.c_int32),
+                ("auto_tuning", ctypes.c_int32), ("allocated_ram_mib", ctypes.c_int32)]
+
+
+CNN_EXEC_PARALLEL, CNN_EXEC_GRAPH = 0, 1
 _descp = ctypes.POINTER(cnn_layer_desc)
 lib.cnn_net_out_shape.argtypes = [_descp, _i, _i, _i, _i, _i, _ip, _ip, _ip]
 lib.cnn_net_workspace_bytes.argtypes = [_descp, _i, _i, _i, _i, _i]
@@ -66,6 +78,11 @@ lib.cnn_net_fwd.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_siz
 lib.cnn_net_fwd_timed.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
                                   ctypes.POINTER(ctypes.c_void_p), _p]
 lib.cnn_conv2d_fwd_config.argtypes = lib.cnn_conv2d_fwd.argtypes[:17] + [_i, _p]
+lib.cnn_netfile_parse.argtypes = [ctypes.c_char_p, _descp, _i, _ip, ctypes.POINTER(cnn_netfile_config)]
+lib.cnn_net_graph_create.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
+                                     ctypes.POINTER(ctypes.c_void_p)]
+lib.cnn_net_graph_launch.argtypes = [_p, _p]
+lib.cnn_net_graph_destroy.argtypes = [_p]
 lib.cnn_conv2d_num_configs.argtypes = []
 lib.cnn_conv2d_config_name.argtypes = [_i]
 lib.cnn_conv2d_config_name.restype = ctypes.c_char_p
@@ -80,7 +97,8 @@ for _name in ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "c
               "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_softmax_fwd", "cnn_net_out_shape",
               "cnn_net_fwd",
               "cnn_net_fwd_timed", "cnn_conv2d_fwd_config", "cnn_conv2d_num_configs",
-              "cnn_set_autotune", "cnn_tuning_import", "cnn_tuning_clear"):
+              "cnn_set_autotune", "cnn_tuning_import", "cnn_tuning_clear", "cnn_netfile_parse",
+              "cnn_net_graph_create", "cnn_net_graph_launch", "cnn_net_graph_destroy"):
     getattr(lib, _name).restype = _i
 
 EXPORTED = ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
@@ -88,7 +106,8 @@ EXPORTED = ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn
             "cnn_net_workspace_bytes", "cnn_net_fwd", "cnn_net_fwd_timed", "cnn_last_error",
             "cnn_version", "cnn_conv2d_num_configs", "cnn_conv2d_config_name",
             "cnn_conv2d_fwd_config", "cnn_set_autotune", "cnn_tuning_export",
-            "cnn_tuning_import", "cnn_tuning_clear")
+            "cnn_tuning_import", "cnn_tuning_clear", "cnn_netfile_parse", "cnn_net_graph_create",
+            "cnn_net_graph_launch", "cnn_net_graph_destroy")
 
 
 class CnnError(RuntimeError):
@@ -270,6 +289,70 @@ def cnn_softmax_fwd(x, y=None, stream=None):
     return y
 
 
+# ---------------------------------------------------------------- NetFile
+@dataclass(frozen=True)
+class NetFile:
+    """A parsed NetFile (cnn_netfile_parse): engine parameters and the layer
+    list, as a ``workloads.Net`` whose layers carry the shapes that the
+    library's own shape rules give for the declared input."""
+
+    net: "_wl.Net"
+    execution_mode: str
+    auto_tuning: bool
+    allocated_ram_mib: int
+
+
+def parse_netfile(text: str, name: str = "netfile", input_chw: Optional[Tuple[int, int, int]] = None,
+                  weight_std: float = 0.01, bias_std: float = 0.01) -> NetFile:
+    """Parses NetFile text.  input_chw overrides (or supplies) the "input"
+    statement; weight_std / bias_std only describe synthetic parameters."""
+    raw = text.encode()
+    n = ctypes.c_int()
+    cfg = cnn_netfile_config()
+    _ok(lib.cnn_netfile_parse(raw, None, 0, ctypes.byref(n), ctypes.byref(cfg)))
+    descs = (cnn_layer_desc * max(n.value, 1))()
+    _ok(lib.cnn_netfile_parse(raw, descs, n.value, ctypes.byref(n), ctypes.byref(cfg)))
+    chw = input_chw or (cfg.in_channels, cfg.in_height, cfg.in_width)
+    if min(chw) <= 0:
+        raise ValueError("NetFile: no input shape (an 'input C H W' line or input_chw=)")
+    layers = []
+    shape = tuple(chw)
+    oc, oh, ow = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    for i in range(n.value):
+        d = descs[i]
+        c, h, w = shape
+        if d.type == CNN_LAYER_CONV:
+            layers.append(_wl.conv(c, d.out_channels, (d.kernel_h, d.kernel_w), (d.stride_h, d.stride_w),
+                                   (d.pad_h, d.pad_w), d.groups, bool(d.fuse_relu)))
+        elif d.type == CNN_LAYER_FC:
+            layers.append(_wl.fc(c * h * w, d.out_channels, bool(d.fuse_relu)))
+        elif d.type == CNN_LAYER_POOL:
+            layers.append(_wl.pool("max" if d.pool_mode == CNN_POOL_MAX else "avg", (d.kernel_h, d.kernel_w),
+                                   (d.stride_h, d.stride_w), (d.pad_h, d.pad_w), bool(d.ceil_mode),
+                                   bool(d.fuse_relu)))
+        elif d.type == CNN_LAYER_LRN:
+            layers.append(_wl.lrn(d.lrn_size, d.lrn_alpha, d.lrn_beta, d.lrn_k))
+        elif d.type == CNN_LAYER_RELU:
+            layers.append(_wl.relu())
+        else:
+            layers.append(_wl.softmax())
+        # shape after this layer, by the library's rules (also checks in=)
+        _ok(lib.cnn_net_out_shape(descs, i + 1, 1, *chw, ctypes.byref(oc), ctypes.byref(oh),
+                                  ctypes.byref(ow)))
+        shape = (oc.value, oh.value, ow.value)
+    net = _wl.Net(name, tuple(chw), tuple(layers), weight_std, bias_std)
+    mode = "graph" if cfg.execution_mode == CNN_EXEC_GRAPH else "parallel"
+    return NetFile(net, mode, bool(cfg.auto_tuning), cfg.allocated_ram_mib)
+
+
+def load_netfile(path: str, **kw) -> NetFile:
+    with open(path) as f:
+        return parse_netfile(f.read(), name=os.path.splitext(os.path.basename(path))[0], **kw)
+
+
+NETFILE_DIR = os.path.join(HERE, "netfiles")
+
+
 # ---------------------------------------------------------------- networks
 class Network:
     """A layer-descriptor array bound to device-resident parameters.
@@ -278,9 +361,22 @@ class Network:
     copied to the device once (loading is outside the timed path, as in the
     paper's measurements).  ``pool_index=True`` allocates an int32 index
     output for every max-pooling layer (per batch size, on first use).
+
+    execution_mode (the NetFile parameter): "parallel" enqueues the layers on
+    every call (cnn_net_fwd); "graph" runs the first call for a given
+    (input, output, batch) eagerly, captures it into a HIP graph
+    (cnn_net_graph_create) and replays the graph from then on.  In graph mode
+    an output allocated by the call (y=None) is a buffer reused by later
+    calls of the same batch size.
     """
 
-    def __init__(self, net, params, device="cuda", pool_index: bool = False):
+    def __init__(self, net, params, device="cuda", pool_index: bool = False,
+                 execution_mode: str = "parallel"):
+        if execution_mode not in ("parallel", "graph"):
+            raise ValueError(f"execution_mode {execution_mode!r}: parallel or graph")
+        self.execution_mode = execution_mode
+        self._graphs: Dict[tuple, ctypes.c_void_p] = {}
+        self._outs: Dict[int, torch.Tensor] = {}
         self.net = net
         self.device = torch.device(device)
         self.weights: List[Tuple[Optional[torch.Tensor], Optional[torch.Tensor]]] = []
@@ -349,9 +445,32 @@ class Network:
             raise CnnError(CNN_ERR_INVALID, cnn_last_error())
         return int(n)
 
+    @classmethod
+    def from_netfile(cls, netfile, params, device="cuda", pool_index: bool = False) -> "Network":
+        """A Network for a parsed NetFile (or NetFile text): its execution
+        mode, and auto-tuning switched on for the library when it asks so."""
+        if isinstance(netfile, str):
+            netfile = parse_netfile(netfile)
+        if netfile.auto_tuning:
+            cnn_set_autotune(True)
+        return cls(netfile.net, params, device, pool_index, netfile.execution_mode)
+
+    def close(self) -> None:
+        """Destroys the captured graphs."""
+        for g in self._graphs.values():
+            lib.cnn_net_graph_destroy(g)
+        self._graphs.clear()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:  # interpreter shutdown
+            pass
+
     def _prepare(self, N: int):
         key = N
         if self._ws_key != key:
+            self.close()  # graphs hold the old workspace and index buffers
             nbytes = self.workspace_bytes(N)
             self._ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
             self._ws_key = key
@@ -378,10 +497,28 @@ class Network:
         """cnn_net_fwd (or cnn_net_fwd_timed with one torch.cuda.Event per layer + 1)."""
         N, C, H, W = x.shape
         self._prepare(N)
+        graph = self.execution_mode == "graph" and events is None
         if y is None:
-            y = torch.empty(self.out_shape(N), dtype=torch.float32, device=x.device)
+            if graph:
+                if N not in self._outs:
+                    self._outs[N] = torch.empty(self.out_shape(N), dtype=torch.float32, device=x.device)
+                y = self._outs[N]
+            else:
+                y = torch.empty(self.out_shape(N), dtype=torch.float32, device=x.device)
         args = (self.descs, len(self.descs), _dev(x, "x"), N, C, H, W, _dev(y, "y"),
                 self._ws.data_ptr(), self._ws.numel())
+        if graph:
+            key = (N, C, H, W, x.data_ptr(), y.data_ptr())
+            g = self._graphs.get(key)
+            if g is None:
+                # eager first pass: validates, and tunes new shapes when auto-tuning is on
+                _ok(lib.cnn_net_fwd(*args, _stream(stream)))
+                g = ctypes.c_void_p()
+                _ok(lib.cnn_net_graph_create(*args, ctypes.byref(g)))
+                self._graphs[key] = g
+                return y
+            _ok(lib.cnn_net_graph_launch(g, _stream(stream)))
+            return y
         if events is None:
             _ok(lib.cnn_net_fwd(*args, _stream(stream)))
         else:

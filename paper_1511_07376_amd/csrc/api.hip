@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -140,8 +141,10 @@ struct Plan {
     PoolShape pool;
 };
 
+// need_weights: the net is about to run (shape queries take descriptors
+// without parameters).
 int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* plan,
-             int64_t* max_elems) {
+             int64_t* max_elems, bool need_weights = true) {
     if (!L || n <= 0) return fail(CNN_ERR_INVALID, "net: no layers");
     if (N < 0 || C <= 0 || H <= 0 || W <= 0)
         return fail(CNN_ERR_INVALID, "net: input %dx%dx%dx%d", N, C, H, W);
@@ -157,7 +160,8 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
         int rc = CNN_OK;
         switch (d.type) {
             case CNN_LAYER_CONV: {
-                if (!d.weight) return fail(CNN_ERR_INVALID, "net layer %d: conv without weights", i);
+                if (need_weights && !d.weight)
+                    return fail(CNN_ERR_INVALID, "net layer %d: conv without weights", i);
                 if (d.in_channels != 0 && d.in_channels != c)
                     return fail(CNN_ERR_INVALID, "net layer %d: conv expects %d input channels, gets %d",
                                 i, d.in_channels, c);
@@ -169,7 +173,8 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
                 break;
             }
             case CNN_LAYER_FC: {
-                if (!d.weight) return fail(CNN_ERR_INVALID, "net layer %d: fc without weights", i);
+                if (need_weights && !d.weight)
+                    return fail(CNN_ERR_INVALID, "net layer %d: fc without weights", i);
                 const int64_t I = (int64_t)c * h * w;
                 if (d.in_features != 0 && d.in_features != I)
                     return fail(CNN_ERR_INVALID, "net layer %d: fc expects %d inputs, gets %dx%dx%d = %lld",
@@ -387,7 +392,7 @@ int cnn_net_out_shape(const cnn_layer_desc* layers, int n_layers, int N, int C, 
     if (n_layers > 4096) return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n_layers);
     std::vector<Plan> plan((size_t)std::max(n_layers, 0));
     int64_t mx;
-    int rc = plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx);
+    int rc = plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx, false);
     if (rc) return rc;
     *outC = plan[n_layers - 1].outC;
     *outH = plan[n_layers - 1].outH;
@@ -399,7 +404,7 @@ size_t cnn_net_workspace_bytes(const cnn_layer_desc* layers, int n_layers, int N
     if (n_layers > 4096 || n_layers <= 0) return 0;
     std::vector<Plan> plan((size_t)n_layers);
     int64_t mx;
-    if (plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx)) return 0;
+    if (plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx, false)) return 0;
     return 2 * align_up((size_t)mx * sizeof(float));
 }
 
@@ -413,6 +418,71 @@ int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x
                       cnn_stream_t stream) {
     if (!events) return fail(CNN_ERR_INVALID, "net_fwd_timed: null events");
     return run_net(layers, n_layers, x, N, C, H, W, y, ws, ws_bytes, events, as_stream(stream));
+}
+
+}  // extern "C"
+
+struct cnn_net_graph {
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;  // null for an empty batch
+};
+
+extern "C" {
+
+int cnn_net_graph_create(const cnn_layer_desc* layers, int n_layers, const float* x, int N, int C,
+                         int H, int W, float* y, void* ws, size_t ws_bytes, cnn_net_graph** graph) {
+    if (!graph) return fail(CNN_ERR_INVALID, "net_graph: null output handle");
+    *graph = nullptr;
+    auto* g = new (std::nothrow) cnn_net_graph;
+    if (!g) return fail(CNN_ERR_INVALID, "net_graph: out of host memory");
+    if (N == 0) {  // validate only: the replay does nothing
+        std::vector<Plan> plan((size_t)std::max(n_layers, 0));
+        int64_t mx;
+        if (n_layers > 4096) { delete g; return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n_layers); }
+        const int rc = plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx);
+        if (rc) { delete g; return rc; }
+        *graph = g;
+        return CNN_OK;
+    }
+    hipStream_t cs;
+    if (hipStreamCreateWithFlags(&cs, hipStreamNonBlocking) != hipSuccess) {
+        delete g;
+        return check_launch("hipStreamCreateWithFlags");
+    }
+    int rc = CNN_OK;
+    if (hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+        rc = check_launch("hipStreamBeginCapture");
+    } else {
+        rc = run_net(layers, n_layers, x, N, C, H, W, y, ws, ws_bytes, nullptr, cs);
+        const hipError_t e = hipStreamEndCapture(cs, &g->graph);
+        if (rc == CNN_OK && e != hipSuccess) rc = fail(CNN_ERR_HIP, "hipStreamEndCapture: %s", hipGetErrorString(e));
+    }
+    if (rc == CNN_OK && hipGraphInstantiate(&g->exec, g->graph, nullptr, nullptr, 0) != hipSuccess)
+        rc = check_launch("hipGraphInstantiate");
+    (void)hipStreamDestroy(cs);
+    if (rc != CNN_OK) {
+        if (g->graph) (void)hipGraphDestroy(g->graph);
+        delete g;
+        return rc;
+    }
+    *graph = g;
+    return CNN_OK;
+}
+
+int cnn_net_graph_launch(cnn_net_graph* graph, cnn_stream_t stream) {
+    if (!graph) return fail(CNN_ERR_INVALID, "net_graph: null handle");
+    if (!graph->exec) return CNN_OK;
+    if (hipGraphLaunch(graph->exec, as_stream(stream)) != hipSuccess) return check_launch("hipGraphLaunch");
+    return CNN_OK;
+}
+
+int cnn_net_graph_destroy(cnn_net_graph* graph) {
+    if (!graph) return CNN_OK;
+    int rc = CNN_OK;
+    if (graph->exec && hipGraphExecDestroy(graph->exec) != hipSuccess) rc = check_launch("hipGraphExecDestroy");
+    if (graph->graph && hipGraphDestroy(graph->graph) != hipSuccess) rc = check_launch("hipGraphDestroy");
+    delete graph;
+    return rc;
 }
 
 const char* cnn_last_error(void) { return g_err; }

@@ -170,3 +170,26 @@ def test_nets_with_softmax(gpu):
         # criterion on the logits becomes a relative one on the output
         np.testing.assert_allclose(y, ref, rtol=1e-4, atol=1e-30)
         np.testing.assert_allclose(y.astype(np.float64).sum(axis=1), 1.0, rtol=1e-5)
+
+
+@pytest.mark.parametrize("mode", ["parallel", "graph"])
+def test_alexnet_from_netfile(gpu, mode):
+    """The shipped AlexNet NetFile, run in each execution mode, against the
+    oracle on sampled images of a batch of 16."""
+    import os
+    print(f"alexnet netfile {mode}", flush=True)
+    text = open(os.path.join(gpu.NETFILE_DIR, "alexnet.txt")).read().replace(
+        "execution_mode parallel", f"execution_mode {mode}")
+    nf = gpu.parse_netfile(text, weight_std=0.01, bias_std=0.01)
+    assert nf.execution_mode == mode
+    params = wl.make_params(nf.net, 10)
+    x = wl.make_input(nf.net, 16, 10)
+    xd = to_dev(x)
+    try:
+        model = gpu.Network.from_netfile(nf, params)   # the file asks for auto-tuning
+        for _ in range(2):                              # graph mode: capture, then replay
+            y = to_host(model(xd))
+            assert_gemm_close(y[[0, 15]], oracle.net_fwd(nf.net, x[[0, 15]], params), 4096,
+                              f"netfile {mode}")
+    finally:
+        gpu.cnn_set_autotune(False)
