@@ -130,8 +130,22 @@ conv2d_igemm_f32(ConvParams p) {
     const int g = blockIdx.z % p.G;
     const int kbeg = (blockIdx.z / p.G) * p.kchunk;  // first tap of this chunk
     const int klen = min(p.kchunk, p.Kr - kbeg);      // taps in this chunk
-    const int m0 = blockIdx.x * TN;
-    const int k0 = blockIdx.y * TM;
+    // Workgroup -> tile.  A launch's workgroups go to the 8 XCDs in turn by
+    // linear id, and each XCD has its own L2: the tiles that read the same
+    // input (every channel tile of a pixel tile, and neighbouring pixel
+    // tiles, whose windows overlap) are given to workgroups of one XCD, in
+    // channel-tile-fastest order.  Ids past the last multiple of 8 keep their
+    // position.
+    int m0, k0;
+    {
+        const int gy = gridDim.y;
+        const int tiles = gridDim.x * gy;
+        const int wg = blockIdx.x + gridDim.x * blockIdx.y;
+        const int full = tiles & ~7;
+        const int seq = wg < full ? (wg & 7) * (full >> 3) + (wg >> 3) : wg;
+        m0 = (seq / gy) * TN;
+        k0 = (seq % gy) * TM;
+    }
 
     // ---- gather setup: this thread's pixel and tap run (fixed for all slabs)
     const int mloc = tid % TN;
