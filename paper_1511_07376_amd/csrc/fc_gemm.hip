@@ -6,11 +6,20 @@
 // [O][I]), so the workgroup stages a TM x BK slab of X and a TN x BK slab of
 // W in LDS with 128-bit loads.  The image index is the MFMA row and the
 // output feature the MFMA column: the 32 lanes of a row write 32 consecutive
-// outputs.  A batch of 16 to 256 images gives few output tiles, far fewer
-// than the chip's 256 compute units, so the reduction is split across
-// workgroups (grid z); the partial sums are added with fp32 atomics into an
-// output pre-filled with the bias, and a ReLU, when the layer has one, runs
-// after the last partial sum has landed.
+// outputs.
+//
+// W is read exactly once and comes from HBM, far away in latency compared
+// with the matrix-core time of one slab, so each thread keeps D slabs of loads
+// in flight in a register ring (slab s + D is requested as slab s is stored to
+// LDS).  The loads go through buffer resources: an index past the matrix gets
+// an out-of-range offset that reads 0, so the loads carry no branches and the
+// compiler can wait for exactly the slab it needs rather than for all of them.
+//
+// A batch of 1 to 256 images gives few output tiles, far fewer than the
+// chip's 256 compute units, so the reduction is split across workgroups
+// (grid z); the partial sums are added with fp32 atomics into an output
+// pre-filled with the bias, and a ReLU, when the layer has one, runs after the
+// last partial sum has landed.
 #include "common.h"
 
 #include <algorithm>
@@ -19,6 +28,9 @@ namespace cnn {
 namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kOutOfRange = (int)0x80000000u;  // buffer offset that reads as 0
 
 struct FcParams {
     const float* x;
@@ -26,45 +38,47 @@ struct FcParams {
     const float* bias;
     float* y;
     int N, I, O;
-    int kchunk;  // reduction length per split (multiple of BK)
+    int kchunk;  // reduction length per split (a multiple of D * BK)
     int relu;
 };
 
-// Loads rows [r0, r0 + tile rows) x columns [kslab, kslab + BK) of a row-major
-// matrix with leading dimension ld into registers, zero outside rows_total
-// and kend.  Thread tid takes items tid, tid + NT, ... of the tile.
-template <int NVEC, int TOT, int NT, int BK, bool VEC>
-__device__ inline void load_tile(const float* base, int ld, int rows_total, int r0, int kslab,
-                                 int kend, int tid, float* reg) {
-    constexpr int VW = VEC ? 4 : 1;
+// Loads rows [0, rows) x columns [kslab, kslab + BK) of the row-major matrix
+// behind `rs` (leading dimension ld; columns past kend and rows past `rows`
+// read as 0) into registers.  Thread tid takes items tid, tid + NT, ... of
+// VW floats (4: 128-bit loads, which need ld and the bases 16-byte aligned).
+template <int NVEC, int TOT, int NT, int BK, int VW>
+__device__ inline void load_tile(__amdgpu_buffer_rsrc_t rs, int ld, int rows, int kslab, int kend,
+                                 int tid, float* reg) {
 #pragma unroll
     for (int i = 0; i < NVEC; ++i) {
         const int idx = tid + i * NT;
-        if (TOT % NT != 0 && idx >= TOT) break;
         const int row = idx / (BK / VW);
-        const int col = (idx % (BK / VW)) * VW;
-        const int gr = r0 + row, kk = kslab + col;
-        if constexpr (VEC) {
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (gr < rows_total && kk < kend)
-                v = *reinterpret_cast<const float4*>(base + (size_t)gr * ld + kk);
-            reg[4 * i] = v.x; reg[4 * i + 1] = v.y; reg[4 * i + 2] = v.z; reg[4 * i + 3] = v.w;
+        const int kk = kslab + (idx % (BK / VW)) * VW;
+        const bool ok = (TOT % NT == 0 || idx < TOT) && row < rows && kk < kend;
+        const int voff = ok ? (row * ld + kk) * 4 : kOutOfRange;
+        if constexpr (VW == 4) {
+            // Cast the whole vector: a bit-cast of one element of an
+            // ext_vector lvalue reads element 0 with this compiler.
+            const f32x4 v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, 0, 0));
+            reg[4 * i] = v[0];
+            reg[4 * i + 1] = v[1];
+            reg[4 * i + 2] = v[2];
+            reg[4 * i + 3] = v[3];
         } else {
-            reg[i] = (gr < rows_total && kk < kend) ? base[(size_t)gr * ld + kk] : 0.0f;
+            reg[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, 0, 0));
         }
     }
 }
 
-template <int NVEC, int TOT, int NT, int BK, int LDK, bool VEC>
+template <int NVEC, int TOT, int NT, int BK, int LDK, int VW>
 __device__ inline void store_tile(float* dst, int tid, const float* reg) {
-    constexpr int VW = VEC ? 4 : 1;
 #pragma unroll
     for (int i = 0; i < NVEC; ++i) {
         const int idx = tid + i * NT;
         if (TOT % NT != 0 && idx >= TOT) break;
         const int row = idx / (BK / VW);
         const int col = (idx % (BK / VW)) * VW;
-        if constexpr (VEC)
+        if constexpr (VW == 4)
             *reinterpret_cast<float4*>(dst + row * LDK + col) =
                 make_float4(reg[4 * i], reg[4 * i + 1], reg[4 * i + 2], reg[4 * i + 3]);
         else
@@ -72,17 +86,18 @@ __device__ inline void store_tile(float* dst, int tid, const float* reg) {
     }
 }
 
-template <int WMW, int WNW, int FM, int FN, int BK, bool VEC, bool SPLIT>
+template <int WMW, int WNW, int FM, int FN, int BK, int D, bool VEC, bool SPLIT>
 __global__ void __launch_bounds__(64 * WMW * WNW)
 fc_gemm_f32(FcParams p) {
     constexpr int TM = WMW * FM * 32;  // images per workgroup
     constexpr int TN = WNW * FN * 32;  // output features per workgroup
     constexpr int NT = 64 * WMW * WNW;
-    constexpr int LDK = BK + 4;
-    constexpr int VW = VEC ? 4 : 1;                // floats per load
+    constexpr int LDK = BK + 4;        // padded LDS row (conflict-free 128-bit reads)
+    constexpr int VW = VEC ? 4 : 1;    // floats per load
     constexpr int ATOT = TM * BK / VW, BTOT = TN * BK / VW;
     constexpr int AV = (ATOT + NT - 1) / NT, BV = (BTOT + NT - 1) / NT;
     static_assert(BK % 8 == 0, "slab must split into two halves of float4s");
+    static_assert(D % 2 == 0, "the two LDS buffers alternate within a round of D slabs");
 
     __shared__ __attribute__((aligned(16))) float sA[2][TM * LDK];  // X [n][i]
     __shared__ __attribute__((aligned(16))) float sB[2][TN * LDK];  // W [o][i]
@@ -91,9 +106,14 @@ fc_gemm_f32(FcParams p) {
     const int n0 = blockIdx.y * TM;
     const int o0 = blockIdx.x * TN;
     const int kbeg = blockIdx.z * p.kchunk;
-    const int kend = min(p.I, kbeg + p.kchunk);
-
-    float ra[AV * VW], rb[BV * VW];
+    const int klen = min(p.I - kbeg, p.kchunk);  // this split's reduction length
+    const int xrows = min(TM, p.N - n0);
+    const int wrows = min(TN, p.O - o0);
+    // resources based at this workgroup's first row and first tap
+    const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(p.x + (size_t)n0 * p.I + kbeg), (short)0, 0x7fffffff, 0x00020000);
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(p.w + (size_t)o0 * p.I + kbeg), (short)0, 0x7fffffff, 0x00020000);
 
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -139,27 +159,31 @@ fc_gemm_f32(FcParams p) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][t], b[j][t], acc[i][j], 0, 0, 0);
     };
 
-    const int nslab = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
-    if (nslab > 0) {
-        load_tile<AV, ATOT, NT, BK, VEC>(p.x, p.I, p.N, n0, kbeg, kend, tid, ra);
-        load_tile<BV, BTOT, NT, BK, VEC>(p.w, p.I, p.O, o0, kbeg, kend, tid, rb);
-        store_tile<AV, ATOT, NT, BK, LDK, VEC>(sA[0], tid, ra);
-        store_tile<BV, BTOT, NT, BK, LDK, VEC>(sB[0], tid, rb);
-        __syncthreads();
+    // Register ring of D slabs.  Round r handles slabs rD .. rD + D - 1: slab
+    // s is stored to LDS buffer s % 2 (its loads were issued D slabs
+    // earlier), then slab s + D is requested into the same registers and slab
+    // s is multiplied.  The barrier after a store also guarantees that
+    // nobody still reads that buffer for slab s - 2.  kchunk is a multiple of
+    // D * BK; only the last split can end inside a round, where the slabs past
+    // its end read as zeros.
+    float ra[D][AV * VW], rb[D][BV * VW];
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+        load_tile<AV, ATOT, NT, BK, VW>(xres, p.I, xrows, j * BK, klen, tid, ra[j]);
+        load_tile<BV, BTOT, NT, BK, VW>(wres, p.I, wrows, j * BK, klen, tid, rb[j]);
     }
-    for (int sl = 0; sl < nslab; ++sl) {
-        const int cur = sl & 1;
-        const bool more = sl + 1 < nslab;
-        if (more) {
-            load_tile<AV, ATOT, NT, BK, VEC>(p.x, p.I, p.N, n0, kbeg + (sl + 1) * BK, kend, tid, ra);
-            load_tile<BV, BTOT, NT, BK, VEC>(p.w, p.I, p.O, o0, kbeg + (sl + 1) * BK, kend, tid, rb);
+    const int nround = klen > 0 ? (klen + D * BK - 1) / (D * BK) : 0;
+    for (int r = 0; r < nround; ++r) {
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            const int knext = (r * D + j + D) * BK;
+            store_tile<AV, ATOT, NT, BK, LDK, VW>(sA[j & 1], tid, ra[j]);
+            store_tile<BV, BTOT, NT, BK, LDK, VW>(sB[j & 1], tid, rb[j]);
+            __syncthreads();
+            load_tile<AV, ATOT, NT, BK, VW>(xres, p.I, xrows, knext, klen, tid, ra[j]);
+            load_tile<BV, BTOT, NT, BK, VW>(wres, p.I, wrows, knext, klen, tid, rb[j]);
+            compute(j & 1);
         }
-        compute(cur);
-        if (more) {
-            store_tile<AV, ATOT, NT, BK, LDK, VEC>(sA[cur ^ 1], tid, ra);
-            store_tile<BV, BTOT, NT, BK, LDK, VEC>(sB[cur ^ 1], tid, rb);
-        }
-        __syncthreads();
     }
 
 #pragma unroll
@@ -194,19 +218,19 @@ __global__ void fc_fill_bias(float* y, const float* bias, int N, int O) {
         y[i] = bias ? bias[i % O] : 0.0f;
 }
 
-template <int WMW, int WNW, int FM, int FN, int BK>
-int launch_fc_cfg(const FcParams& prm0, bool vec, hipStream_t st) {
+// target: workgroups to aim for (the chip holds two to four of these per
+// compute unit at once).
+template <int WMW, int WNW, int FM, int FN, int BK, int D, bool VEC>
+int launch_fc_cfg(const FcParams& prm0, int target, hipStream_t st) {
     constexpr int TM = WMW * FM * 32;
     constexpr int TN = WNW * FN * 32;
+    constexpr int UNIT = D * BK;  // reduction granule of one split
     FcParams prm = prm0;
     const int tiles = ceil_div(prm.N, TM) * ceil_div(prm.O, TN);
-    // Enough workgroups to cover the 256 compute units about twice, but keep
-    // at least four slabs of reduction per workgroup.
-    int splits = ceil_div(512, tiles);
-    const int max_splits = std::max(1, prm.I / (4 * BK));
-    if (splits > max_splits) splits = max_splits;
-    if (splits < 1) splits = 1;
-    prm.kchunk = ceil_div(ceil_div(prm.I, splits), BK) * BK;
+    // enough splits to reach the target, but at least two rounds per split
+    int splits = std::min(ceil_div(target, tiles), std::max(1, prm.I / (2 * UNIT)));
+    splits = std::max(splits, 1);
+    prm.kchunk = ceil_div(ceil_div(prm.I, splits), UNIT) * UNIT;
     splits = ceil_div(prm.I, prm.kchunk);
     dim3 grid(ceil_div(prm.O, TN), ceil_div(prm.N, TM), splits);
     dim3 block(64 * WMW * WNW);
@@ -214,19 +238,13 @@ int launch_fc_cfg(const FcParams& prm0, bool vec, hipStream_t st) {
         const int total = prm.N * prm.O;
         hipLaunchKernelGGL(fc_fill_bias, dim3(std::min(ceil_div(total, 256), 2048)), dim3(256), 0, st,
                            prm.y, prm.bias, prm.N, prm.O);
-        if (vec)
-            hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, true, true>), grid, block, 0, st, prm);
-        else
-            hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, false, true>), grid, block, 0, st, prm);
+        hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, true>), grid, block, 0, st, prm);
         int rc = check_launch("fc_gemm_f32");
         if (rc != CNN_OK) return rc;
         if (prm.relu) return launch_relu(prm.y, prm.y, (int64_t)prm.N * prm.O, st);
         return CNN_OK;
     }
-    if (vec)
-        hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, true, false>), grid, block, 0, st, prm);
-    else
-        hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, false, false>), grid, block, 0, st, prm);
+    hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, false>), grid, block, 0, st, prm);
     return check_launch("fc_gemm_f32");
 }
 
@@ -235,6 +253,9 @@ int launch_fc_cfg(const FcParams& prm0, bool vec, hipStream_t st) {
 int launch_fc(const float* x, int N, int I, const float* w, const float* bias, int O, int relu,
               float* y, hipStream_t st) {
     if (N == 0) return CNN_OK;
+    // buffer offsets within a workgroup's rows are 31-bit
+    if ((int64_t)128 * I * 4 >= ((int64_t)1 << 31))
+        return fail(CNN_ERR_UNSUPPORTED, "fc: %d input features exceed this kernel's 2^22 limit", I);
     FcParams prm;
     prm.x = x;
     prm.w = w;
@@ -247,9 +268,13 @@ int launch_fc(const float* x, int N, int I, const float* w, const float* bias, i
     prm.relu = relu;
     const bool vec = (I % 4 == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0) &&
                      ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
-    if (N <= 32) return launch_fc_cfg<1, 4, 1, 1, 32>(prm, vec, st);   // 32 x 128
-    if (N <= 64) return launch_fc_cfg<1, 4, 2, 1, 32>(prm, vec, st);   // 64 x 128
-    return launch_fc_cfg<2, 2, 2, 2, 16>(prm, vec, st);                // 128 x 128
+    const int target = N <= 64 ? 512 : 1024;
+    if (N <= 32)  // 32 images x 128 features
+        return vec ? launch_fc_cfg<1, 4, 1, 1, 32, 4, true>(prm, target, st)
+                   : launch_fc_cfg<1, 4, 1, 1, 32, 4, false>(prm, target, st);
+    // 64 x 64
+    return vec ? launch_fc_cfg<2, 2, 1, 1, 16, 4, true>(prm, target, st)
+               : launch_fc_cfg<2, 2, 1, 1, 16, 4, false>(prm, target, st);
 }
 
 }  // namespace cnn
