@@ -17,8 +17,8 @@
 // branches.
 //
 // Workgroup tile: TM output channels x TN output pixels, reduction in slabs of
-// BK taps, double-buffered in LDS (the loads of slab s+1 are in flight while
-// slab s feeds the matrix cores).  Each wave owns FM x FN blocks of 32x32
+// BK taps, double-buffered in LDS, with the loads of slabs s+1 and s+2 in
+// flight in two register stages while slab s feeds the matrix cores.  Each wave owns FM x FN blocks of 32x32
 // accumulated with v_mfma_f32_32x32x2_f32.  The output channel is the MFMA
 // row and the output pixel the MFMA column, so the 32 lanes of a row store 32
 // consecutive pixels: NCHW stores are coalesced.
@@ -62,24 +62,6 @@ struct ConvParams {
     int splits;  // reduction chunks; > 1: partial tiles are added atomically
     int kchunk;  // taps per chunk (a multiple of every slab length; Kr if splits == 1)
 };
-
-// Instruction-scheduling pattern of one slab (LLVM sched_group_barrier masks:
-// 0x008 matrix core, 0x100 LDS read, 0x020 memory read, 0x002 vector ALU,
-// 0x004 scalar ALU, 0x200 LDS write): the fragment reads first, then each
-// matrix-core instruction followed by a share of the next slab's loads and
-// address arithmetic, then the LDS writes.
-template <int NMFMA, int NDSREAD, int NVMEM>
-__device__ inline void schedule_slab() {
-    __builtin_amdgcn_sched_group_barrier(0x100, NDSREAD, 0);
-#pragma unroll
-    for (int i = 0; i < NMFMA; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if (i < NVMEM) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
-        __builtin_amdgcn_sched_group_barrier(0x004, 5, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x200, 16, 0);
-}
 
 // Gather modes.
 //  kGatherScalar: taps decoded and advanced in scalar registers, bounds
@@ -170,10 +152,10 @@ conv2d_igemm_f32(ConvParams p) {
 
     const int nslab = (klen + BK - 1) / BK;
     const int niter = (nslab + KS - 1) / KS;  // slabs per group
-    extern __shared__ __attribute__((aligned(16))) int stab[];  // (niter + 1) * KS * BK entries
+    extern __shared__ __attribute__((aligned(16))) int stab[];  // (niter + 2) * KS * BK entries
     unsigned inv = 0xffffffffu;
     if constexpr (GATHER != kGatherScalar) {
-        for (int kk = threadIdx.x; kk < (niter + 1) * KS * BK; kk += NTB) {
+        for (int kk = threadIdx.x; kk < (niter + 2) * KS * BK; kk += NTB) {
             int e = GATHER == kGatherMask ? 31 : (int)0x80000000u;
             if (kk < klen) {
                 const int c = (kbeg + kk) / p.RS;
@@ -198,8 +180,8 @@ conv2d_igemm_f32(ConvParams p) {
     }
     if constexpr (GATHER != kGatherScalar) __syncthreads();
 
-    float xr[KRUN];
-    auto load_x = [&](int kslab) {
+    float xr[2][KRUN];  // two register stages
+    auto load_x = [&](int kslab, int sg) {
         const int kk0 = kslab + kgrp * KRUN;  // uniform
         if constexpr (GATHER != kGatherScalar) {
 #pragma unroll
@@ -215,7 +197,7 @@ conv2d_igemm_f32(ConvParams p) {
                     } else {
                         voff = (int)((unsigned)lane_off + (unsigned)es[u]);
                     }
-                    xr[j + u] =
+                    xr[sg][j + u] =
                         __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, voff, 0, 0));
                 }
             }
@@ -232,7 +214,7 @@ conv2d_igemm_f32(ConvParams p) {
             const bool ok = (kk0 + j < klen) && ((unsigned)(hb + r) < (unsigned)p.H) &&
                             ((unsigned)(wb + s) < (unsigned)p.W);
             const int voff = ok ? lane_off + toff : kOutOfRange;
-            xr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, voff, 0, 0));
+            xr[sg][j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, voff, 0, 0));
             // next tap: s, then r, then c
             ++s;
             toff += 4;
@@ -245,11 +227,12 @@ conv2d_igemm_f32(ConvParams p) {
             toff += wrap_r ? (p.HW - p.R * p.W) * 4 : 0;
         }
     };
-    auto store_x = [&](int buf) {
+    auto store_x = [&](int buf, int sg) {
         float* dst = sB(buf) + mloc * LDK + kgrp * KRUN;
 #pragma unroll
         for (int j = 0; j < KRUN; j += 4)
-            *reinterpret_cast<float4*>(dst + j) = make_float4(xr[j], xr[j + 1], xr[j + 2], xr[j + 3]);
+            *reinterpret_cast<float4*>(dst + j) =
+                make_float4(xr[sg][j], xr[sg][j + 1], xr[sg][j + 2], xr[sg][j + 3]);
     };
 
     // ---- weight tile loads: rows k0.. of the group's [Kg][Kr] block, through a
@@ -269,8 +252,8 @@ conv2d_igemm_f32(ConvParams p) {
         w_off[i] = w_rowok[i] ? ((g * p.Kg + k0 + row) * p.Kr + kbeg + w_col[i]) * 4 : 0;
         w_lds[i] = row * LDK + w_col[i];
     }
-    float wr[WV * VW];
-    auto load_w = [&](int kslab) {
+    float wr[2][WV * VW];
+    auto load_w = [&](int kslab, int sg) {
 #pragma unroll
         for (int i = 0; i < WV; ++i) {
             if constexpr (VEC_W) {
@@ -281,25 +264,25 @@ conv2d_igemm_f32(ConvParams p) {
                 typedef float f32x4 __attribute__((ext_vector_type(4)));
                 const f32x4 v =
                     __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(wres, voff, 0, 0));
-                wr[4 * i] = v[0];
-                wr[4 * i + 1] = v[1];
-                wr[4 * i + 2] = v[2];
-                wr[4 * i + 3] = v[3];
+                wr[sg][4 * i] = v[0];
+                wr[sg][4 * i + 1] = v[1];
+                wr[sg][4 * i + 2] = v[2];
+                wr[sg][4 * i + 3] = v[3];
             } else {
                 const bool ok = w_rowok[i] && (kslab + w_col[i] < klen);
                 const int voff = ok ? w_off[i] + kslab * 4 : kOutOfRange;
-                wr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wres, voff, 0, 0));
+                wr[sg][i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wres, voff, 0, 0));
             }
         }
     };
-    auto store_w = [&](int buf) {
+    auto store_w = [&](int buf, int sg) {
 #pragma unroll
         for (int i = 0; i < WV; ++i) {
             if constexpr (VEC_W)
                 *reinterpret_cast<float4*>(sA(buf) + w_lds[i]) =
-                    make_float4(wr[4 * i], wr[4 * i + 1], wr[4 * i + 2], wr[4 * i + 3]);
+                    make_float4(wr[sg][4 * i], wr[sg][4 * i + 1], wr[sg][4 * i + 2], wr[sg][4 * i + 3]);
             else
-                sA(buf)[w_lds[i]] = wr[i];
+                sA(buf)[w_lds[i]] = wr[sg][i];
         }
     };
 
@@ -348,27 +331,40 @@ conv2d_igemm_f32(ConvParams p) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][t], b[j][t], acc[i][j], 0, 0, 0);
     };
 
-    // ---- main loop: slab s computes from LDS while slab s+1 loads from memory
-    // The body is one basic block: the last iteration loads a slab past the
-    // reduction (all zeros) into the idle buffer, which nothing reads.  The
-    // scheduling hints spread the next slab's loads and address arithmetic
-    // between the matrix-core instructions of the current slab, so that the
-    // wave keeps issuing while the matrix core works.
-    load_x(sgrp * BK);
-    load_w(sgrp * BK);
-    store_x(0);
-    store_w(0);
-    __syncthreads();
-    for (int it = 0; it < niter; ++it) {
-        const int cur = it & 1;
-        load_x(((it + 1) * KS + sgrp) * BK);
-        load_w(((it + 1) * KS + sgrp) * BK);
-        compute(cur);
-        store_x(cur ^ 1);
-        store_w(cur ^ 1);
-        schedule_slab<FM * FN * (BK / 2), (FM + FN) * (BK / 8), KRUN + WV>();
+    // ---- main loop: slab s computes from LDS while slabs s+1 and s+2 load.
+    // Two slabs of loads in flight.  Slab s is stored to LDS buffer s % 2 from
+    // register stage s % 2, then slab s + 2 is requested into that stage and
+    // slab s is multiplied.  One barrier per slab, which also guarantees that
+    // nobody still reads the buffer for slab s - 2.  An odd last slab runs
+    // after the loop, so that the loop body is straight-line code and each
+    // store waits only for its own slab's loads.
+    auto slab_k = [&](int it) { return (it * KS + sgrp) * BK; };  // first tap of group slab it
+    load_x(slab_k(0), 0);
+    load_w(slab_k(0), 0);
+    load_x(slab_k(1), 1);
+    load_w(slab_k(1), 1);
+    int it = 0;
+    for (; it + 1 < niter; it += 2) {
+        store_x(0, 0);
+        store_w(0, 0);
         __syncthreads();
+        load_x(slab_k(it + 2), 0);
+        load_w(slab_k(it + 2), 0);
+        compute(0);
+        store_x(1, 1);
+        store_w(1, 1);
+        __syncthreads();
+        load_x(slab_k(it + 3), 1);
+        load_w(slab_k(it + 3), 1);
+        compute(1);
     }
+    if (it < niter) {
+        store_x(0, 0);
+        store_w(0, 0);
+        __syncthreads();
+        compute(0);
+    }
+    if constexpr (KS > 1) __syncthreads();  // the group reduction reuses the tile buffers
 
     // ---- sum the slab groups' partial tiles (lanes on consecutive words)
     if constexpr (KS > 1) {
@@ -440,7 +436,7 @@ int launch_cfg(const ConvParams& prm, bool vec_w, hipStream_t st) {
     dim3 grid(ceil_div(prm.M, TN), ceil_div(prm.Kg, TM), prm.G * prm.splits);
     dim3 block(64 * WMW * WNW * KS);
     // tap tables are at most 32 KiB of LDS
-    const int tab_entries = (ceil_div(ceil_div(prm.kchunk, BK), KS) + 1) * KS * BK;
+    const int tab_entries = (ceil_div(ceil_div(prm.kchunk, BK), KS) + 2) * KS * BK;
     const bool tab_fits = tab_entries * 4 <= 32768;
     int mode = kGatherScalar;
     if (tab_fits && prm.ph == 0 && prm.pw == 0)
