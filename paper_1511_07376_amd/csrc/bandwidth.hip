@@ -165,9 +165,9 @@ __global__ void __launch_bounds__(kThreads) avgpool_f32(PoolParams p) {
 
 // ------------------------------------------------------------------ LRN
 // One thread per (n, chunk of CCH channels, pixel); lanes cover consecutive
-// pixels.  The thread walks its channels keeping the HALF values on each
-// side of the current channel in registers, so it reads each of its
-// channels once plus a halo of HALF channels on each side of the chunk.
+// pixels.  The thread loads its CCH channels plus a halo of HALF channels on
+// each side into registers at once (every load in flight together), then
+// forms each channel's window sum from registers.
 // Splitting the channels into chunks gives the launch enough threads to keep
 // HBM busy even for the 27x27 layers.
 struct LrnParams {
@@ -188,34 +188,34 @@ __device__ inline float pow_neg(float scale, float beta) {
 template <int HALF, int CCH>
 __global__ void __launch_bounds__(kThreads) lrn_across_f32(LrnParams p) {
     constexpr int WIN = 2 * HALF + 1;
+    constexpr int NV = CCH + 2 * HALF;  // channels read per thread
+    // Channels outside [0, C) get an out-of-range buffer offset and read 0:
+    // the NV loads carry no branch, so all of them are in flight at once.
+    const __amdgpu_buffer_rsrc_t xres =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.x), (short)0, 0x7fffffff, 0x00020000);
     for (int t = blockIdx.x * kThreads + threadIdx.x; t < p.total; t += gridDim.x * kThreads) {
         const int hw = t % p.HW;
         const int rest = t / p.HW;
         const int chunk = rest % p.nchunk;
         const int n = rest / p.nchunk;
         const int c0 = chunk * CCH;
-        const float* xp = p.x + n * p.C * p.HW + hw;
-        float* yp = p.y + n * p.C * p.HW + hw;
-        // win[j] holds channel c - HALF + j (0 outside [0, C))
-        float win[WIN];
+        const int base = n * p.C * p.HW + hw;  // element (n, 0, hw)
+        float v[NV];                            // v[j]: channel c0 - HALF + j
 #pragma unroll
-        for (int j = 0; j < WIN; ++j) {
-            const int cc = c0 + j - HALF;
-            win[j] = (cc >= 0 && cc < p.C) ? xp[cc * p.HW] : 0.0f;
+        for (int j = 0; j < NV; ++j) {
+            const int cc = c0 - HALF + j;
+            const int off = (unsigned)cc < (unsigned)p.C ? (base + cc * p.HW) * 4 : (int)0x80000000u;
+            v[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0));
         }
+        float* yp = p.y + base;
 #pragma unroll
         for (int i = 0; i < CCH; ++i) {
-            const int c = c0 + i;
-            if (c >= p.C) break;
+            // window of channel c0 + i: v[i] .. v[i + 2 HALF]
             float sq = 0.0f;
 #pragma unroll
-            for (int j = 0; j < WIN; ++j) sq += win[j] * win[j];
+            for (int j = 0; j < WIN; ++j) sq += v[i + j] * v[i + j];
             const float scale = p.k + p.alpha_over_size * sq;
-            yp[c * p.HW] = win[HALF] * pow_neg(scale, p.beta);
-#pragma unroll
-            for (int j = 0; j < WIN - 1; ++j) win[j] = win[j + 1];
-            const int cn = c + HALF + 1;
-            win[WIN - 1] = cn < p.C ? xp[cn * p.HW] : 0.0f;
+            if (c0 + i < p.C) yp[(c0 + i) * p.HW] = v[i + HALF] * pow_neg(scale, p.beta);
         }
     }
 }
@@ -322,24 +322,35 @@ int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha
     p.k = k;
     if (N == 0) return CNN_OK;
     constexpr int kChunk = 32;
-    if (size / 2 > 4) {  // wide windows: recompute each window sum
+    const int64_t img = (int64_t)C * p.HW;
+    if (size / 2 > 4 || img >= ((int64_t)1 << 29)) {  // wide windows, huge images
         p.nchunk = 1;
         p.total = N * p.HW;
         hipLaunchKernelGGL(lrn_across_any_f32, dim3(grid_for(p.total)), dim3(kThreads), 0, st, p,
                            size / 2);
         return check_launch("lrn_across_any_f32");
     }
+    // The chunked kernel addresses x through a buffer resource with 31-bit
+    // byte offsets: fewer than 2^29 elements per launch (whole images).
+    const int per_launch = (int)std::min<int64_t>(N, (((int64_t)1 << 29) - 1) / img);
     p.nchunk = ceil_div(C, kChunk);
-    p.total = N * p.nchunk * p.HW;
-    const dim3 grid(grid_for(p.total)), block(kThreads);
-    switch (size / 2) {
-        case 0: hipLaunchKernelGGL((lrn_across_f32<0, kChunk>), grid, block, 0, st, p); break;
-        case 1: hipLaunchKernelGGL((lrn_across_f32<1, kChunk>), grid, block, 0, st, p); break;
-        case 2: hipLaunchKernelGGL((lrn_across_f32<2, kChunk>), grid, block, 0, st, p); break;
-        case 3: hipLaunchKernelGGL((lrn_across_f32<3, kChunk>), grid, block, 0, st, p); break;
-        default: hipLaunchKernelGGL((lrn_across_f32<4, kChunk>), grid, block, 0, st, p); break;
+    for (int n0 = 0; n0 < N; n0 += per_launch) {
+        const int nb = std::min(per_launch, N - n0);
+        p.x = x + (size_t)n0 * img;
+        p.y = y + (size_t)n0 * img;
+        p.total = nb * p.nchunk * p.HW;
+        const dim3 grid(grid_for(p.total)), block(kThreads);
+        switch (size / 2) {
+            case 0: hipLaunchKernelGGL((lrn_across_f32<0, kChunk>), grid, block, 0, st, p); break;
+            case 1: hipLaunchKernelGGL((lrn_across_f32<1, kChunk>), grid, block, 0, st, p); break;
+            case 2: hipLaunchKernelGGL((lrn_across_f32<2, kChunk>), grid, block, 0, st, p); break;
+            case 3: hipLaunchKernelGGL((lrn_across_f32<3, kChunk>), grid, block, 0, st, p); break;
+            default: hipLaunchKernelGGL((lrn_across_f32<4, kChunk>), grid, block, 0, st, p); break;
+        }
+        const int rc = check_launch("lrn_across_f32");
+        if (rc != CNN_OK) return rc;
     }
-    return check_launch("lrn_across_f32");
+    return CNN_OK;
 }
 
 int launch_relu(const float* x, float* y, int64_t n, hipStream_t st) {

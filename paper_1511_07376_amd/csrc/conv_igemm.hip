@@ -15,7 +15,7 @@ struct ConvConfig {
     LaunchFn launch;
 };
 
-#define CNN_CONV_ENTRY(I, WMW, WNW, FM, FN, BK, KS)                                        \
+#define CNN_CONV_ENTRY(I, WMW, WNW, FM, FN, BK, KS, ST)                                        \
     ConvConfig{#WMW "x" #WNW " waves, " #FM "x" #FN " blocks, BK " #BK ", " #KS " slab groups",      \
                WMW * FM * 32, WNW * FN * 32, BK, 64 * WMW * WNW * KS, &launch_c##I},
 

@@ -82,9 +82,10 @@ constexpr int kGatherScalar = 0, kGatherMask = 1, kGatherNoPad = 2;
 // output tile; their partial tiles are summed through LDS before the
 // epilogue.  This gives small-pixel-count layers more waves without
 // shrinking each wave's tile.
-template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W, int GATHER, int KS>
+template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W, int GATHER, int KS, int ST>
 __global__ void __launch_bounds__(64 * WMW * WNW * KS)
 conv2d_igemm_f32(ConvParams p) {
+    static_assert(ST % 2 == 0, "the two LDS buffers alternate within a round of ST slabs");
     constexpr int TM = WMW * FM * 32;  // output channels per workgroup
     constexpr int TN = WNW * FN * 32;  // output pixels per workgroup
     constexpr int NT = 64 * WMW * WNW;  // threads per slab group
@@ -152,10 +153,10 @@ conv2d_igemm_f32(ConvParams p) {
 
     const int nslab = (klen + BK - 1) / BK;
     const int niter = (nslab + KS - 1) / KS;  // slabs per group
-    extern __shared__ __attribute__((aligned(16))) int stab[];  // (niter + 2) * KS * BK entries
+    extern __shared__ __attribute__((aligned(16))) int stab[];  // (niter + ST) * KS * BK entries
     unsigned inv = 0xffffffffu;
     if constexpr (GATHER != kGatherScalar) {
-        for (int kk = threadIdx.x; kk < (niter + 2) * KS * BK; kk += NTB) {
+        for (int kk = threadIdx.x; kk < (niter + ST) * KS * BK; kk += NTB) {
             int e = GATHER == kGatherMask ? 31 : (int)0x80000000u;
             if (kk < klen) {
                 const int c = (kbeg + kk) / p.RS;
@@ -180,7 +181,7 @@ conv2d_igemm_f32(ConvParams p) {
     }
     if constexpr (GATHER != kGatherScalar) __syncthreads();
 
-    float xr[2][KRUN];  // two register stages
+    float xr[ST][KRUN];  // register stages
     auto load_x = [&](int kslab, int sg) {
         const int kk0 = kslab + kgrp * KRUN;  // uniform
         if constexpr (GATHER != kGatherScalar) {
@@ -252,7 +253,7 @@ conv2d_igemm_f32(ConvParams p) {
         w_off[i] = w_rowok[i] ? ((g * p.Kg + k0 + row) * p.Kr + kbeg + w_col[i]) * 4 : 0;
         w_lds[i] = row * LDK + w_col[i];
     }
-    float wr[2][WV * VW];
+    float wr[ST][WV * VW];
     auto load_w = [&](int kslab, int sg) {
 #pragma unroll
         for (int i = 0; i < WV; ++i) {
@@ -331,38 +332,40 @@ conv2d_igemm_f32(ConvParams p) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][t], b[j][t], acc[i][j], 0, 0, 0);
     };
 
-    // ---- main loop: slab s computes from LDS while slabs s+1 and s+2 load.
-    // Two slabs of loads in flight.  Slab s is stored to LDS buffer s % 2 from
-    // register stage s % 2, then slab s + 2 is requested into that stage and
-    // slab s is multiplied.  One barrier per slab, which also guarantees that
-    // nobody still reads the buffer for slab s - 2.  An odd last slab runs
-    // after the loop, so that the loop body is straight-line code and each
-    // store waits only for its own slab's loads.
+    // ---- main loop: slab s computes from LDS while slabs s+1 .. s+ST load.
+    // ST slabs of loads in flight (ST register stages).  Slab s is stored to
+    // LDS buffer s % 2 from register stage s % ST, then slab s + ST is
+    // requested into that stage and slab s is multiplied.  One barrier per
+    // slab, which also guarantees that nobody still reads the buffer for slab
+    // s - 2.  The last niter % ST slabs run after the loop, so that the loop
+    // body is straight-line code and each store waits only for its own slab's
+    // loads.
     auto slab_k = [&](int it) { return (it * KS + sgrp) * BK; };  // first tap of group slab it
-    load_x(slab_k(0), 0);
-    load_w(slab_k(0), 0);
-    load_x(slab_k(1), 1);
-    load_w(slab_k(1), 1);
-    int it = 0;
-    for (; it + 1 < niter; it += 2) {
-        store_x(0, 0);
-        store_w(0, 0);
-        __syncthreads();
-        load_x(slab_k(it + 2), 0);
-        load_w(slab_k(it + 2), 0);
-        compute(0);
-        store_x(1, 1);
-        store_w(1, 1);
-        __syncthreads();
-        load_x(slab_k(it + 3), 1);
-        load_w(slab_k(it + 3), 1);
-        compute(1);
+#pragma unroll
+    for (int j = 0; j < ST; ++j) {
+        load_x(slab_k(j), j);
+        load_w(slab_k(j), j);
     }
-    if (it < niter) {
-        store_x(0, 0);
-        store_w(0, 0);
-        __syncthreads();
-        compute(0);
+    int it = 0;
+    for (; it + ST - 1 < niter; it += ST) {
+#pragma unroll
+        for (int j = 0; j < ST; ++j) {
+            store_x(j & 1, j);
+            store_w(j & 1, j);
+            __syncthreads();
+            load_x(slab_k(it + j + ST), j);
+            load_w(slab_k(it + j + ST), j);
+            compute(j & 1);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < ST - 1; ++j) {
+        if (it + j < niter) {
+            store_x(j & 1, j);
+            store_w(j & 1, j);
+            __syncthreads();
+            compute(j & 1);
+        }
     }
     if constexpr (KS > 1) __syncthreads();  // the group reduction reuses the tile buffers
 
@@ -423,20 +426,20 @@ conv2d_igemm_f32(ConvParams p) {
 // ---------------------------------------------------------------- configurations
 typedef int (*LaunchFn)(const ConvParams&, bool vec_w, hipStream_t st);
 
-template <int WMW, int WNW, int FM, int FN, int BK, int KS, bool VEC_W, int GATHER>
+template <int WMW, int WNW, int FM, int FN, int BK, int KS, int ST, bool VEC_W, int GATHER>
 inline void launch_kernel(const ConvParams& prm, dim3 grid, dim3 block, size_t shm, hipStream_t st) {
-    hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, VEC_W, GATHER, KS>), grid, block, shm, st, prm);
+    hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, VEC_W, GATHER, KS, ST>), grid, block, shm, st, prm);
 }
 
 // Picks the gather mode for the shape and launches one configuration.
-template <int WMW, int WNW, int FM, int FN, int BK, int KS>
+template <int WMW, int WNW, int FM, int FN, int BK, int KS, int ST>
 int launch_cfg(const ConvParams& prm, bool vec_w, hipStream_t st) {
     constexpr int TM = WMW * FM * 32;
     constexpr int TN = WNW * FN * 32;
     dim3 grid(ceil_div(prm.M, TN), ceil_div(prm.Kg, TM), prm.G * prm.splits);
     dim3 block(64 * WMW * WNW * KS);
     // tap tables are at most 32 KiB of LDS
-    const int tab_entries = (ceil_div(ceil_div(prm.kchunk, BK), KS) + 2) * KS * BK;
+    const int tab_entries = (ceil_div(ceil_div(prm.kchunk, BK), KS) + ST) * KS * BK;
     const bool tab_fits = tab_entries * 4 <= 32768;
     int mode = kGatherScalar;
     if (tab_fits && prm.ph == 0 && prm.pw == 0)
@@ -445,46 +448,46 @@ int launch_cfg(const ConvParams& prm, bool vec_w, hipStream_t st) {
         mode = kGatherMask;
     const size_t shm = mode == kGatherScalar ? 0 : (size_t)tab_entries * 4;
     if (vec_w) {
-        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, true, kGatherNoPad>(prm, grid, block, shm, st);
-        else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, true, kGatherMask>(prm, grid, block, shm, st);
-        else launch_kernel<WMW, WNW, FM, FN, BK, KS, true, kGatherScalar>(prm, grid, block, shm, st);
+        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherNoPad>(prm, grid, block, shm, st);
+        else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherMask>(prm, grid, block, shm, st);
+        else launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherScalar>(prm, grid, block, shm, st);
     } else {
-        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, false, kGatherNoPad>(prm, grid, block, shm, st);
-        else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, false, kGatherMask>(prm, grid, block, shm, st);
-        else launch_kernel<WMW, WNW, FM, FN, BK, KS, false, kGatherScalar>(prm, grid, block, shm, st);
+        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherNoPad>(prm, grid, block, shm, st);
+        else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherMask>(prm, grid, block, shm, st);
+        else launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherScalar>(prm, grid, block, shm, st);
     }
     return check_launch("conv2d_igemm_f32");
 }
 
 // The configurations: index, waves along output channels, waves along
 // pixels, 32x32 blocks per wave along channels and pixels, slab length,
-// slab groups per workgroup.
+// slab groups per workgroup, register stages of slabs in flight.
 #define CNN_CONV_CONFIGS(X)      \
-    X(0, 2, 2, 2, 2, 16, 1)  /* 128 x 128 */  \
-    X(1, 2, 2, 2, 2, 32, 1)  /* 128 x 128 */  \
-    X(2, 4, 1, 1, 2, 16, 1)  /* 128 x 64 */   \
-    X(3, 4, 1, 1, 2, 32, 1)  /* 128 x 64 */   \
-    X(4, 1, 4, 2, 1, 16, 1)  /* 64 x 128 */   \
-    X(5, 1, 4, 2, 1, 32, 1)  /* 64 x 128 */   \
-    X(6, 1, 4, 3, 1, 16, 1)  /* 96 x 128 */   \
-    X(7, 1, 4, 3, 1, 32, 1)  /* 96 x 128 */   \
-    X(8, 1, 4, 1, 1, 16, 1)  /* 32 x 128 */   \
-    X(9, 2, 2, 1, 1, 16, 1)  /* 64 x 64 */    \
-    X(10, 2, 2, 1, 1, 32, 1) /* 64 x 64 */    \
-    X(11, 2, 4, 2, 2, 16, 1) /* 128 x 256, 8 waves */ \
-    X(12, 1, 2, 3, 2, 16, 1) /* 96 x 128, 2 waves */  \
-    X(13, 2, 1, 2, 2, 16, 1) /* 128 x 64, 2 waves */  \
-    X(14, 2, 2, 1, 1, 16, 2) /* 64 x 64, 2 slab groups of 4 waves */  \
-    X(15, 2, 1, 2, 2, 16, 2) /* 128 x 64, 2 slab groups of 2 waves */
+    X(0, 2, 2, 2, 2, 16, 1, 2)  /* 128 x 128 */  \
+    X(1, 2, 2, 2, 2, 32, 1, 2)  /* 128 x 128 */  \
+    X(2, 4, 1, 1, 2, 16, 1, 2)  /* 128 x 64 */   \
+    X(3, 4, 1, 1, 2, 32, 1, 2)  /* 128 x 64 */   \
+    X(4, 1, 4, 2, 1, 16, 1, 2)  /* 64 x 128 */   \
+    X(5, 1, 4, 2, 1, 32, 1, 2)  /* 64 x 128 */   \
+    X(6, 1, 4, 3, 1, 16, 1, 2)  /* 96 x 128 */   \
+    X(7, 1, 4, 3, 1, 32, 1, 2)  /* 96 x 128 */   \
+    X(8, 1, 4, 1, 1, 16, 1, 2)  /* 32 x 128 */   \
+    X(9, 2, 2, 1, 1, 16, 1, 2)  /* 64 x 64 */    \
+    X(10, 2, 2, 1, 1, 32, 1, 2) /* 64 x 64 */    \
+    X(11, 2, 4, 2, 2, 16, 1, 2) /* 128 x 256, 8 waves */ \
+    X(12, 1, 2, 3, 2, 16, 1, 2) /* 96 x 128, 2 waves */  \
+    X(13, 2, 1, 2, 2, 16, 1, 2) /* 128 x 64, 2 waves */  \
+    X(14, 2, 2, 1, 1, 16, 2, 2) /* 64 x 64, 2 slab groups of 4 waves */  \
+    X(15, 2, 1, 2, 2, 16, 2, 2) /* 128 x 64, 2 slab groups of 2 waves */
 
-#define CNN_CONV_DECLARE(I, WMW, WNW, FM, FN, BK, KS) \
+#define CNN_CONV_DECLARE(I, WMW, WNW, FM, FN, BK, KS, ST) \
     int launch_c##I(const ConvParams& prm, bool vec_w, hipStream_t st);
 CNN_CONV_CONFIGS(CNN_CONV_DECLARE)
 
 // Defines launch_c<I> (one translation unit per group of configurations).
-#define CNN_CONV_DEFINE(I, WMW, WNW, FM, FN, BK, KS)                               \
+#define CNN_CONV_DEFINE(I, WMW, WNW, FM, FN, BK, KS, ST)                           \
     int launch_c##I(const ConvParams& prm, bool vec_w, hipStream_t st) {           \
-        return launch_cfg<WMW, WNW, FM, FN, BK, KS>(prm, vec_w, st);               \
+        return launch_cfg<WMW, WNW, FM, FN, BK, KS, ST>(prm, vec_w, st);           \
     }
 
 }  // namespace conv
