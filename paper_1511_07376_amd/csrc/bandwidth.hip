@@ -86,14 +86,17 @@ pool_staged_f32(PoolParams p, int planes_per_block, int nplanes, FastDiv fpq, Fa
     const int HW = p.H * p.W, PQ = p.P * p.Q;
     for (int pl0 = blockIdx.x * planes_per_block; pl0 < nplanes; pl0 += gridDim.x * planes_per_block) {
         const int np = min(planes_per_block, nplanes - pl0);
-        const float* src = p.x + (size_t)pl0 * HW;
         const int len = np * HW;
-        {  // len <= 16 * kThreads: every load of the run is in flight at once
+        {  // len <= 16 * kThreads: every load of the run is in flight at once.
+           // The buffer resource covers exactly the run, so loads past its end
+           // read 0 without a branch.
+            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<float*>(p.x + (size_t)pl0 * HW), (short)0, len * 4, 0x00020000);
             float v[16];
 #pragma unroll
             for (int u = 0; u < 16; ++u) {
                 const int i = threadIdx.x + u * kThreads;
-                v[u] = i < len ? src[i] : 0.0f;
+                v[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, i * 4, 0, 0));
             }
 #pragma unroll
             for (int u = 0; u < 16; ++u) {
