@@ -255,6 +255,7 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
 
     const float* cur = x;
     int next_buf = 0;
+    bool relu_pending = false;  // cur still needs the previous FC layer's ReLU
     for (int i = 0; i < n; ++i) {
         if (events) {
             if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), st) != hipSuccess)
@@ -271,9 +272,18 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
             case CNN_LAYER_CONV:
                 rc = conv2d_dispatch(p.conv, cur, d.weight, d.bias, p.relu, out, st);
                 break;
-            case CNN_LAYER_FC:
-                rc = launch_fc(cur, N, p.inC * p.inH * p.inW, d.weight, d.bias, p.outC, p.relu, out, st);
+            case CNN_LAYER_FC: {
+                // A ReLU after a split-reduction FC layer whose output only feeds
+                // another FC layer is applied as that layer reads its input.
+                int nx = i + 1;
+                while (nx < n && plan[nx].skipped) ++nx;
+                const bool next_fc = nx < n && plan[nx].type == CNN_LAYER_FC;
+                const bool relu_in = relu_pending;
+                relu_pending = false;
+                rc = launch_fc(cur, N, p.inC * p.inH * p.inW, d.weight, d.bias, p.outC, p.relu, out, st,
+                               relu_in, next_fc ? &relu_pending : nullptr);
                 break;
+            }
             case CNN_LAYER_POOL:
                 rc = launch_pool(p.pool, d.pool_mode, p.relu, cur, out, d.pool_index, st);
                 break;

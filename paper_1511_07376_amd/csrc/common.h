@@ -48,8 +48,11 @@ const char* conv2d_config_name(int i);
 // first when auto-tuning is on and the shape is new).
 int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const float* bias,
                     int relu, float* y, hipStream_t st);
+// relu_in: apply a ReLU to x as it is read.  relu_left non-null: when the
+// layer's ReLU would need a pass of its own (split reduction), skip it and set
+// *relu_left, so that the caller can fold it into the next layer's input.
 int launch_fc(const float* x, int N, int I, const float* w, const float* bias, int O, int relu,
-              float* y, hipStream_t st);
+              float* y, hipStream_t st, bool relu_in = false, bool* relu_left = nullptr);
 int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y, int32_t* idx,
                 hipStream_t st);
 int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha, float beta,

@@ -70,8 +70,11 @@ __device__ inline void load_tile(__amdgpu_buffer_rsrc_t rs, int ld, int rows, in
     }
 }
 
-template <int NVEC, int TOT, int NT, int BK, int LDK, int VW>
+// RELU: store max(v, 0) (the input of a layer whose producer's ReLU was
+// deferred to its consumer).
+template <int NVEC, int TOT, int NT, int BK, int LDK, int VW, bool RELU = false>
 __device__ inline void store_tile(float* dst, int tid, const float* reg) {
+    auto r = [](float v) { return RELU ? (v > 0.0f ? v : 0.0f) : v; };
 #pragma unroll
     for (int i = 0; i < NVEC; ++i) {
         const int idx = tid + i * NT;
@@ -80,13 +83,14 @@ __device__ inline void store_tile(float* dst, int tid, const float* reg) {
         const int col = (idx % (BK / VW)) * VW;
         if constexpr (VW == 4)
             *reinterpret_cast<float4*>(dst + row * LDK + col) =
-                make_float4(reg[4 * i], reg[4 * i + 1], reg[4 * i + 2], reg[4 * i + 3]);
+                make_float4(r(reg[4 * i]), r(reg[4 * i + 1]), r(reg[4 * i + 2]), r(reg[4 * i + 3]));
         else
-            dst[row * LDK + col] = reg[i];
+            dst[row * LDK + col] = r(reg[i]);
     }
 }
 
-template <int WMW, int WNW, int FM, int FN, int BK, int D, bool VEC, bool SPLIT>
+// RELU_X: the layer's input is taken through a ReLU.
+template <int WMW, int WNW, int FM, int FN, int BK, int D, bool VEC, bool SPLIT, bool RELU_X>
 __global__ void __launch_bounds__(64 * WMW * WNW)
 fc_gemm_f32(FcParams p) {
     constexpr int TM = WMW * FM * 32;  // images per workgroup
@@ -177,7 +181,7 @@ fc_gemm_f32(FcParams p) {
 #pragma unroll
         for (int j = 0; j < D; ++j) {
             const int knext = (r * D + j + D) * BK;
-            store_tile<AV, ATOT, NT, BK, LDK, VW>(sA[j & 1], tid, ra[j]);
+            store_tile<AV, ATOT, NT, BK, LDK, VW, RELU_X>(sA[j & 1], tid, ra[j]);
             store_tile<BV, BTOT, NT, BK, LDK, VW>(sB[j & 1], tid, rb[j]);
             __syncthreads();
             load_tile<AV, ATOT, NT, BK, VW>(xres, p.I, xrows, knext, klen, tid, ra[j]);
@@ -219,9 +223,9 @@ __global__ void fc_fill_bias(float* y, const float* bias, int N, int O) {
 }
 
 // target: workgroups to aim for (the chip holds two to four of these per
-// compute unit at once).
-template <int WMW, int WNW, int FM, int FN, int BK, int D, bool VEC>
-int launch_fc_cfg(const FcParams& prm0, int target, hipStream_t st) {
+// compute unit at once).  relu_left: see launch_fc.
+template <int WMW, int WNW, int FM, int FN, int BK, int D, bool VEC, bool RELU_X>
+int launch_fc_cfg(const FcParams& prm0, int target, hipStream_t st, bool* relu_left) {
     constexpr int TM = WMW * FM * 32;
     constexpr int TN = WNW * FN * 32;
     constexpr int UNIT = D * BK;  // reduction granule of one split
@@ -238,20 +242,25 @@ int launch_fc_cfg(const FcParams& prm0, int target, hipStream_t st) {
         const int total = prm.N * prm.O;
         hipLaunchKernelGGL(fc_fill_bias, dim3(std::min(ceil_div(total, 256), 2048)), dim3(256), 0, st,
                            prm.y, prm.bias, prm.N, prm.O);
-        hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, true>), grid, block, 0, st, prm);
+        hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, true, RELU_X>), grid, block, 0, st, prm);
         int rc = check_launch("fc_gemm_f32");
         if (rc != CNN_OK) return rc;
+        if (prm.relu && relu_left) {  // the caller applies it
+            *relu_left = true;
+            return CNN_OK;
+        }
         if (prm.relu) return launch_relu(prm.y, prm.y, (int64_t)prm.N * prm.O, st);
         return CNN_OK;
     }
-    hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, false>), grid, block, 0, st, prm);
+    hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, false, RELU_X>), grid, block, 0, st, prm);
     return check_launch("fc_gemm_f32");
 }
 
 }  // namespace
 
 int launch_fc(const float* x, int N, int I, const float* w, const float* bias, int O, int relu,
-              float* y, hipStream_t st) {
+              float* y, hipStream_t st, bool relu_in, bool* relu_left) {
+    if (relu_left) *relu_left = false;
     if (N == 0) return CNN_OK;
     // buffer offsets within a workgroup's rows are 31-bit
     if ((int64_t)128 * I * 4 >= ((int64_t)1 << 31))
@@ -269,12 +278,14 @@ int launch_fc(const float* x, int N, int I, const float* w, const float* bias, i
     const bool vec = (I % 4 == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0) &&
                      ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
     const int target = N <= 64 ? 512 : 1024;
-    if (N <= 32)  // 32 images x 128 features
-        return vec ? launch_fc_cfg<1, 4, 1, 1, 32, 4, true>(prm, target, st)
-                   : launch_fc_cfg<1, 4, 1, 1, 32, 4, false>(prm, target, st);
-    // 64 x 64
-    return vec ? launch_fc_cfg<2, 2, 1, 1, 16, 4, true>(prm, target, st)
-               : launch_fc_cfg<2, 2, 1, 1, 16, 4, false>(prm, target, st);
+#define CNN_FC_CFG(WMW, WNW, FM, FN, BK, D)                                                             \
+    (vec ? (relu_in ? launch_fc_cfg<WMW, WNW, FM, FN, BK, D, true, true>(prm, target, st, relu_left)    \
+                    : launch_fc_cfg<WMW, WNW, FM, FN, BK, D, true, false>(prm, target, st, relu_left))  \
+         : (relu_in ? launch_fc_cfg<WMW, WNW, FM, FN, BK, D, false, true>(prm, target, st, relu_left)   \
+                    : launch_fc_cfg<WMW, WNW, FM, FN, BK, D, false, false>(prm, target, st, relu_left)))
+    if (N <= 32) return CNN_FC_CFG(1, 4, 1, 1, 32, 4);  // 32 images x 128 features
+    return CNN_FC_CFG(2, 2, 1, 1, 16, 4);               // 64 x 64
+#undef CNN_FC_CFG
 }
 
 }  // namespace cnn

@@ -193,3 +193,18 @@ def test_alexnet_from_netfile(gpu, mode):
                               f"netfile {mode}")
     finally:
         gpu.cnn_set_autotune(False)
+
+
+@pytest.mark.parametrize("batch", [1, 17, 70])
+def test_fc_chain_relu_carried_into_next_layer(gpu, batch):
+    """FC+ReLU layers that split their reduction leave the ReLU to the next FC
+    layer, which applies it as it reads its input; half of the pre-activations
+    are negative here, so a lost or doubled ReLU shows."""
+    print(f"fc chain batch {batch}", flush=True)
+    net = wl.Net("fc_chain", (8, 8, 8), (
+        wl.fc(512, 300, relu=True), wl.fc(300, 200), wl.relu(), wl.fc(200, 10),
+    ), 0.2, 0.2, input_dist="normal")
+    x = wl.make_input(net, batch, 11)
+    params = wl.make_params(net, 11)
+    y = to_host(gpu.Network(net, params)(to_dev(x)))
+    assert_gemm_close(y, oracle.net_fwd(net, x, params), 200, f"fc chain B{batch}")
