@@ -137,14 +137,22 @@ struct Plan {
     int outC, outH, outW;  // output shape
     int relu;              // ReLU executed inside this layer
     bool skipped;          // a RELU layer folded into its predecessor
+    bool fc_split;         // FC: the reduction is split (output must start as the bias)
+    size_t fc_off;         // FC with fc_split, not last: byte offset of its output in
+                           // the FC area of the workspace
     ConvShape conv;
     PoolShape pool;
 };
 
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
 // need_weights: the net is about to run (shape queries take descriptors
-// without parameters).
+// without parameters).  *fc_bytes: size of the workspace area that holds the
+// outputs of split-reduction FC layers (other than the last layer), which
+// are all set to their biases by one launch at the start of the pass.
 int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* plan,
-             int64_t* max_elems, bool need_weights = true) {
+             int64_t* max_elems, bool need_weights = true, size_t* fc_bytes = nullptr) {
     if (!L || n <= 0) return fail(CNN_ERR_INVALID, "net: no layers");
     if (N < 0 || C <= 0 || H <= 0 || W <= 0)
         return fail(CNN_ERR_INVALID, "net: input %dx%dx%dx%d", N, C, H, W);
@@ -182,6 +190,7 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
                 if (I > kMaxElems) return fail(CNN_ERR_UNSUPPORTED, "net layer %d: fc input too large", i);
                 rc = check_fc(N, (int)I, d.out_channels);
                 if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
+                p.fc_split = fc_splits(N, (int)I, d.out_channels) > 1;
                 c = d.out_channels; h = 1; w = 1;
                 p.relu = d.fuse_relu != 0;
                 break;
@@ -222,11 +231,18 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
         if (!p.skipped) prev_exec = i;
     }
     *max_elems = mx;
+    int last = n - 1;
+    while (last > 0 && plan[last].skipped) --last;
+    size_t fc = 0;
+    for (int i = 0; i < n; ++i) {
+        if (plan[i].type == CNN_LAYER_FC && plan[i].fc_split && i != last) {
+            plan[i].fc_off = fc;
+            fc += align_up((size_t)N * plan[i].outC * sizeof(float));
+        }
+    }
+    if (fc_bytes) *fc_bytes = fc;
     return CNN_OK;
 }
-
-constexpr size_t kAlign = 256;
-size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H, int W, float* y,
             void* ws, size_t ws_bytes, void* const* events, hipStream_t st) {
@@ -234,7 +250,8 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
     if (n > 4096) return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n);
     std::vector<Plan> plan((size_t)std::max(n, 0));
     int64_t mx = 0;
-    int rc = plan_net(L, n, N, C, H, W, plan.data(), &mx);
+    size_t fc_bytes = 0;
+    int rc = plan_net(L, n, N, C, H, W, plan.data(), &mx, true, &fc_bytes);
     if (rc) return rc;
     if (N == 0) {  // nothing to compute; still honour the event contract
         for (int i = 0; events && i <= n; ++i)
@@ -243,15 +260,30 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
         return CNN_OK;
     }
     const size_t half = align_up((size_t)mx * sizeof(float));
-    if (!ws || ws_bytes < 2 * half)
-        return fail(CNN_ERR_WORKSPACE, "net: workspace of %zu bytes, %zu needed", ws_bytes, 2 * half);
+    if (!ws || ws_bytes < 2 * half + fc_bytes)
+        return fail(CNN_ERR_WORKSPACE, "net: workspace of %zu bytes, %zu needed", ws_bytes,
+                    2 * half + fc_bytes);
     if (reinterpret_cast<uintptr_t>(ws) % 16)
         return fail(CNN_ERR_INVALID, "net: workspace must be 16-byte aligned");
     float* buf[2] = {static_cast<float*>(ws),
                      reinterpret_cast<float*>(static_cast<char*>(ws) + half)};
+    char* fc_area = static_cast<char*>(ws) + 2 * half;
 
     int last = n - 1;
     while (last > 0 && plan[last].skipped) --last;
+
+    // Every split-reduction FC output starts as its bias: one launch for all.
+    {
+        std::vector<FcFill> fills;
+        for (int i = 0; i < n; ++i) {
+            const Plan& p = plan[i];
+            if (p.type != CNN_LAYER_FC || !p.fc_split) continue;
+            float* dst = i == last ? y : reinterpret_cast<float*>(fc_area + p.fc_off);
+            fills.push_back(FcFill{dst, L[i].bias, N, p.outC});
+        }
+        rc = launch_fc_fills(fills.data(), (int)fills.size(), st);
+        if (rc) return rc;
+    }
 
     const float* cur = x;
     int next_buf = 0;
@@ -265,6 +297,8 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
         if (p.skipped) continue;
         const cnn_layer_desc& d = L[i];
         float* out = (i == last) ? y : buf[next_buf];
+        if (p.type == CNN_LAYER_FC && p.fc_split && i != last)
+            out = reinterpret_cast<float*>(fc_area + p.fc_off);
         // an in-place ReLU or softmax keeps its buffer
         if ((p.type == CNN_LAYER_RELU || p.type == CNN_LAYER_SOFTMAX) && i != last && cur != x)
             out = const_cast<float*>(cur);
@@ -281,7 +315,7 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
                 const bool relu_in = relu_pending;
                 relu_pending = false;
                 rc = launch_fc(cur, N, p.inC * p.inH * p.inW, d.weight, d.bias, p.outC, p.relu, out, st,
-                               relu_in, next_fc ? &relu_pending : nullptr);
+                               relu_in, next_fc ? &relu_pending : nullptr, p.fc_split);
                 break;
             }
             case CNN_LAYER_POOL:
@@ -414,8 +448,9 @@ size_t cnn_net_workspace_bytes(const cnn_layer_desc* layers, int n_layers, int N
     if (n_layers > 4096 || n_layers <= 0) return 0;
     std::vector<Plan> plan((size_t)n_layers);
     int64_t mx;
-    if (plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx, false)) return 0;
-    return 2 * align_up((size_t)mx * sizeof(float));
+    size_t fc_bytes = 0;
+    if (plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx, false, &fc_bytes)) return 0;
+    return 2 * align_up((size_t)mx * sizeof(float)) + fc_bytes;
 }
 
 int cnn_net_fwd(const cnn_layer_desc* layers, int n_layers, const float* x, int N, int C, int H,

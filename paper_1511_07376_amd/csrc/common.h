@@ -51,8 +51,22 @@ int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const fl
 // relu_in: apply a ReLU to x as it is read.  relu_left non-null: when the
 // layer's ReLU would need a pass of its own (split reduction), skip it and set
 // *relu_left, so that the caller can fold it into the next layer's input.
+// prefilled: y already holds the bias (see fc_splits, launch_fc_fills).
 int launch_fc(const float* x, int N, int I, const float* w, const float* bias, int O, int relu,
-              float* y, hipStream_t st, bool relu_in = false, bool* relu_left = nullptr);
+              float* y, hipStream_t st, bool relu_in = false, bool* relu_left = nullptr,
+              bool prefilled = false);
+// Reduction splits launch_fc uses for this shape; above 1 its output must
+// start as the bias (launch_fc fills it unless told it is prefilled).
+int fc_splits(int N, int I, int O);
+// y_j[n][o] = bias_j[o] (or 0) for several FC outputs, in one launch per
+// kMaxFcFills jobs.
+constexpr int kMaxFcFills = 8;
+struct FcFill {
+    float* y;
+    const float* bias;
+    int N, O;
+};
+int launch_fc_fills(const FcFill* jobs, int n, hipStream_t st);
 int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y, int32_t* idx,
                 hipStream_t st);
 int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha, float beta,

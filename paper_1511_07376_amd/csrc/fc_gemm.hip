@@ -222,26 +222,59 @@ __global__ void fc_fill_bias(float* y, const float* bias, int N, int O) {
         y[i] = bias ? bias[i % O] : 0.0f;
 }
 
-// target: workgroups to aim for (the chip holds two to four of these per
-// compute unit at once).  relu_left: see launch_fc.
+// Several outputs at once: job j sets y_j[n][o] = bias_j[o] (or 0).
+struct FillJobs {
+    FcFill job[kMaxFcFills];
+    int n;
+};
+
+__global__ void fc_fill_bias_multi(FillJobs f) {
+    for (int j = 0; j < f.n; ++j) {
+        const FcFill& jb = f.job[j];
+        const int total = jb.N * jb.O;
+        for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x)
+            jb.y[i] = jb.bias ? jb.bias[i % jb.O] : 0.0f;
+    }
+}
+
+// Tile and reduction split of an FC layer (one rule for launch_fc and the
+// network planner).
+struct FcGeom {
+    int tm, tn, unit;  // workgroup tile, reduction granule of one split
+    int target;        // workgroups to aim for (two to four per compute unit)
+};
+
+FcGeom fc_geom(int N) {
+    if (N <= 32) return FcGeom{32, 128, 4 * 32, 512};  // launch_fc_cfg<1, 4, 1, 1, 32, 4>
+    return FcGeom{64, 64, 4 * 16, N <= 64 ? 512 : 1024};  // launch_fc_cfg<2, 2, 1, 1, 16, 4>
+}
+
+// Splits and the reduction length per split.
+int fc_split(const FcGeom& g, int N, int I, int O, int* kchunk) {
+    const int tiles = ceil_div(N, g.tm) * ceil_div(O, g.tn);
+    // enough splits to reach the target, but at least two rounds per split
+    int splits = std::min(ceil_div(g.target, tiles), std::max(1, I / (2 * g.unit)));
+    splits = std::max(splits, 1);
+    *kchunk = ceil_div(ceil_div(I, splits), g.unit) * g.unit;
+    return ceil_div(I, *kchunk);
+}
+
+// relu_left, prefilled: see launch_fc.
 template <int WMW, int WNW, int FM, int FN, int BK, int D, bool VEC, bool RELU_X>
-int launch_fc_cfg(const FcParams& prm0, int target, hipStream_t st, bool* relu_left) {
+int launch_fc_cfg(const FcParams& prm0, const FcGeom& g, hipStream_t st, bool* relu_left, bool prefilled) {
     constexpr int TM = WMW * FM * 32;
     constexpr int TN = WNW * FN * 32;
-    constexpr int UNIT = D * BK;  // reduction granule of one split
+    if (g.tm != TM || g.tn != TN || g.unit != D * BK)
+        return fail(CNN_ERR_UNSUPPORTED, "fc: tile geometry out of step with fc_geom");
     FcParams prm = prm0;
-    const int tiles = ceil_div(prm.N, TM) * ceil_div(prm.O, TN);
-    // enough splits to reach the target, but at least two rounds per split
-    int splits = std::min(ceil_div(target, tiles), std::max(1, prm.I / (2 * UNIT)));
-    splits = std::max(splits, 1);
-    prm.kchunk = ceil_div(ceil_div(prm.I, splits), UNIT) * UNIT;
-    splits = ceil_div(prm.I, prm.kchunk);
+    const int splits = fc_split(g, prm.N, prm.I, prm.O, &prm.kchunk);
     dim3 grid(ceil_div(prm.O, TN), ceil_div(prm.N, TM), splits);
     dim3 block(64 * WMW * WNW);
     if (splits > 1) {
         const int total = prm.N * prm.O;
-        hipLaunchKernelGGL(fc_fill_bias, dim3(std::min(ceil_div(total, 256), 2048)), dim3(256), 0, st,
-                           prm.y, prm.bias, prm.N, prm.O);
+        if (!prefilled)
+            hipLaunchKernelGGL(fc_fill_bias, dim3(std::min(ceil_div(total, 256), 2048)), dim3(256), 0, st,
+                               prm.y, prm.bias, prm.N, prm.O);
         hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, true, RELU_X>), grid, block, 0, st, prm);
         int rc = check_launch("fc_gemm_f32");
         if (rc != CNN_OK) return rc;
@@ -258,8 +291,30 @@ int launch_fc_cfg(const FcParams& prm0, int target, hipStream_t st, bool* relu_l
 
 }  // namespace
 
+int fc_splits(int N, int I, int O) {
+    int kchunk;
+    return N > 0 ? fc_split(fc_geom(N), N, I, O, &kchunk) : 1;
+}
+
+int launch_fc_fills(const FcFill* jobs, int n, hipStream_t st) {
+    for (int j0 = 0; j0 < n; j0 += kMaxFcFills) {
+        FillJobs f;
+        f.n = std::min(kMaxFcFills, n - j0);
+        int most = 0;
+        for (int j = 0; j < f.n; ++j) {
+            f.job[j] = jobs[j0 + j];
+            most = std::max(most, f.job[j].N * f.job[j].O);
+        }
+        if (most == 0) continue;
+        hipLaunchKernelGGL(fc_fill_bias_multi, dim3(std::min(ceil_div(most, 256), 2048)), dim3(256), 0, st, f);
+        const int rc = check_launch("fc_fill_bias_multi");
+        if (rc != CNN_OK) return rc;
+    }
+    return CNN_OK;
+}
+
 int launch_fc(const float* x, int N, int I, const float* w, const float* bias, int O, int relu,
-              float* y, hipStream_t st, bool relu_in, bool* relu_left) {
+              float* y, hipStream_t st, bool relu_in, bool* relu_left, bool prefilled) {
     if (relu_left) *relu_left = false;
     if (N == 0) return CNN_OK;
     // buffer offsets within a workgroup's rows are 31-bit
@@ -277,13 +332,13 @@ int launch_fc(const float* x, int N, int I, const float* w, const float* bias, i
     prm.relu = relu;
     const bool vec = (I % 4 == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0) &&
                      ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
-    const int target = N <= 64 ? 512 : 1024;
-#define CNN_FC_CFG(WMW, WNW, FM, FN, BK, D)                                                             \
-    (vec ? (relu_in ? launch_fc_cfg<WMW, WNW, FM, FN, BK, D, true, true>(prm, target, st, relu_left)    \
-                    : launch_fc_cfg<WMW, WNW, FM, FN, BK, D, true, false>(prm, target, st, relu_left))  \
-         : (relu_in ? launch_fc_cfg<WMW, WNW, FM, FN, BK, D, false, true>(prm, target, st, relu_left)   \
-                    : launch_fc_cfg<WMW, WNW, FM, FN, BK, D, false, false>(prm, target, st, relu_left)))
-    if (N <= 32) return CNN_FC_CFG(1, 4, 1, 1, 32, 4);  // 32 images x 128 features
+    const FcGeom g = fc_geom(N);
+#define CNN_FC_CFG(WMW, WNW, FM, FN, BK, D)                                                                  \
+    (vec ? (relu_in ? launch_fc_cfg<WMW, WNW, FM, FN, BK, D, true, true>(prm, g, st, relu_left, prefilled)    \
+                    : launch_fc_cfg<WMW, WNW, FM, FN, BK, D, true, false>(prm, g, st, relu_left, prefilled))  \
+         : (relu_in ? launch_fc_cfg<WMW, WNW, FM, FN, BK, D, false, true>(prm, g, st, relu_left, prefilled)   \
+                    : launch_fc_cfg<WMW, WNW, FM, FN, BK, D, false, false>(prm, g, st, relu_left, prefilled)))
+    if (N <= 32) return CNN_FC_CFG(1, 4, 1, 1, 32, 4);  // 32 images x 128 features (fc_geom)
     return CNN_FC_CFG(2, 2, 1, 1, 16, 4);               // 64 x 64
 #undef CNN_FC_CFG
 }
