@@ -220,7 +220,10 @@ size_t cnn_net_workspace_bytes(const cnn_layer_desc* layers, int n_layers,
  * ([N][outC][outH][outW]).  ws is caller-owned device memory of at least
  * cnn_net_workspace_bytes(); intermediates live there.  A RELU layer that
  * follows a CONV, FC or POOL layer is executed inside that layer (Sec. 3.5);
- * other RELU layers and SOFTMAX layers run in place.  A SOFTMAX layer uses
+ * an LRN layer followed by a POOL layer runs inside that pooling kernel (its
+ * output never goes to memory; the values equal those of the two layers run
+ * separately, bit for bit); other RELU layers and SOFTMAX layers run in
+ * place.  A SOFTMAX layer uses
  * only the type field.  Every layer is validated before the first launch. */
 int cnn_net_fwd(const cnn_layer_desc* layers, int n_layers, const float* x,
                 int N, int C, int H, int W, float* y, void* ws, size_t ws_bytes,
@@ -229,8 +232,9 @@ int cnn_net_fwd(const cnn_layer_desc* layers, int n_layers, const float* x,
 /* As cnn_net_fwd, and records events[i] (hipEvent_t) on the stream before
  * layer i and events[n_layers] after the last one, so that the caller can
  * time each layer (the paper times whole networks and the heaviest conv
- * layer separately, Sec. 4.2).  A RELU layer executed inside its predecessor
- * gets an empty interval. */
+ * layer separately, Sec. 4.2).  A RELU layer executed inside its predecessor,
+ * and an LRN layer executed inside the pooling layer after it, get an empty
+ * interval. */
 int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x,
                       int N, int C, int H, int W, float* y, void* ws,
                       size_t ws_bytes, void* const* events, cnn_stream_t stream);

@@ -136,7 +136,9 @@ struct Plan {
     int inC, inH, inW;     // input shape of the layer (per image)
     int outC, outH, outW;  // output shape
     int relu;              // ReLU executed inside this layer
-    bool skipped;          // a RELU layer folded into its predecessor
+    bool skipped;          // a RELU layer folded into its predecessor, or an LRN
+                           // layer run inside the pooling layer after it
+    int lrn_from;          // POOL: index of the LRN layer it runs first, or -1
     bool fc_split;         // FC: the reduction is split (output must start as the bias)
     size_t fc_off;         // FC with fc_split, not last: byte offset of its output in
                            // the FC area of the workspace
@@ -163,6 +165,7 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
         const cnn_layer_desc& d = L[i];
         Plan& p = plan[i];
         p = Plan{};
+        p.lrn_from = -1;
         p.type = d.type;
         p.inC = c; p.inH = h; p.inW = w;
         int rc = CNN_OK;
@@ -201,6 +204,13 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
                 if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
                 if (d.pool_index && d.pool_mode != CNN_POOL_MAX)
                     return fail(CNN_ERR_INVALID, "net layer %d: indices requested for average pooling", i);
+                // An LRN whose output only feeds this pooling layer runs inside it:
+                // its output never goes to memory.
+                if (prev_exec >= 0 && plan[prev_exec].type == CNN_LAYER_LRN &&
+                    lrn_pool_fusable(p.pool, L[prev_exec].lrn_size)) {
+                    plan[prev_exec].skipped = true;
+                    p.lrn_from = prev_exec;
+                }
                 h = p.pool.P; w = p.pool.Q;
                 p.relu = d.fuse_relu != 0;
                 break;
@@ -319,7 +329,13 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
                 break;
             }
             case CNN_LAYER_POOL:
-                rc = launch_pool(p.pool, d.pool_mode, p.relu, cur, out, d.pool_index, st);
+                if (p.lrn_from >= 0) {  // cur is still the LRN's input
+                    const cnn_layer_desc& ld = L[p.lrn_from];
+                    rc = launch_lrn_pool(p.pool, d.pool_mode, p.relu, ld.lrn_size, ld.lrn_alpha,
+                                         ld.lrn_beta, ld.lrn_k, cur, out, d.pool_index, st);
+                } else {
+                    rc = launch_pool(p.pool, d.pool_mode, p.relu, cur, out, d.pool_index, st);
+                }
                 break;
             case CNN_LAYER_LRN:
                 rc = launch_lrn(cur, N, p.inC, p.inH, p.inW, d.lrn_size, d.lrn_alpha, d.lrn_beta,

@@ -4,6 +4,7 @@
 #include "common.h"
 
 #include <algorithm>
+#include <cmath>
 
 namespace cnn {
 namespace {
@@ -188,6 +189,20 @@ __device__ inline float pow_neg(float scale, float beta) {
     return __builtin_amdgcn_exp2f(-beta * __builtin_amdgcn_logf(scale));
 }
 
+// One LRN output: w[0 .. WIN-1] are channels c - WIN/2 .. c + WIN/2 at one
+// pixel (0 outside the tensor), so w[WIN/2] is x itself.  The standalone and
+// the pooling-fused kernels both go through this function, and its roundings
+// are spelled out (explicit fused multiply-adds, which the compiler may
+// neither split nor share between neighbouring windows), so that the two give
+// the same bits.
+template <int WIN>
+__device__ inline float lrn_value(const float* w, float k, float alpha_over_size, float beta) {
+    float sq = w[0] * w[0];
+#pragma unroll
+    for (int j = 1; j < WIN; ++j) sq = __builtin_fmaf(w[j], w[j], sq);
+    return w[WIN / 2] * pow_neg(__builtin_fmaf(alpha_over_size, sq, k), beta);
+}
+
 template <int HALF, int CCH>
 __global__ void __launch_bounds__(kThreads) lrn_across_f32(LrnParams p) {
     constexpr int WIN = 2 * HALF + 1;
@@ -212,14 +227,136 @@ __global__ void __launch_bounds__(kThreads) lrn_across_f32(LrnParams p) {
         }
         float* yp = p.y + base;
 #pragma unroll
-        for (int i = 0; i < CCH; ++i) {
-            // window of channel c0 + i: v[i] .. v[i + 2 HALF]
-            float sq = 0.0f;
-#pragma unroll
-            for (int j = 0; j < WIN; ++j) sq += v[i + j] * v[i + j];
-            const float scale = p.k + p.alpha_over_size * sq;
-            if (c0 + i < p.C) yp[(c0 + i) * p.HW] = v[i + HALF] * pow_neg(scale, p.beta);
+        for (int i = 0; i < CCH; ++i) {  // window of channel c0 + i: v[i] .. v[i + 2 HALF]
+            if (c0 + i < p.C) yp[(c0 + i) * p.HW] = lrn_value<WIN>(&v[i], p.k, p.alpha_over_size, p.beta);
         }
+    }
+}
+
+// LRN followed by pooling in one pass, for the network executor (an LRN layer
+// whose output only feeds a pooling layer): the LRN output never goes to
+// memory.  A workgroup takes one image, CB channels and a band of PB pooling
+// output rows:
+//   1. loads the band's input rows of its channels plus the LRN halo into LDS
+//      (every load of a thread in flight at once; channels and rows outside
+//      the tensor read 0),
+//   2. computes each LRN value once, in place: a thread walks the channels
+//      of one (row, column) of the band with the window in registers and
+//      writes channel c's value over its input once no later window needs
+//      it (same arithmetic as the LRN kernel),
+//   3. pools from the tile (same order and comparisons as the pooling
+//      kernels), so the result equals the two layers run one after the other,
+//      bit for bit.
+struct LrnPoolParams {
+    const float* x;
+    float* y;
+    int32_t* idx;
+    int C, H, W, P, Q, kh, kw, sh, sw, ph, pw;
+    int CB, PB, RB;   // channels, output rows and input rows per workgroup
+    int nchunk, nband;
+    FastDiv f_plane, f_w, f_pbq, f_q;  // RB*W, W, PB*Q, Q
+    int relu;
+    float alpha_over_size, beta, k;
+};
+
+template <int HALF, int MODE, bool WITH_IDX>  // MODE 0: max, 1: average
+__global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
+    constexpr int WIN = 2 * HALF + 1;
+    extern __shared__ float in[];           // [CB + 2 HALF][RB][W]
+    const int CIN = p.CB + 2 * HALF;        // channels staged
+    int b = blockIdx.x;
+    const int band = b % p.nband;
+    b /= p.nband;
+    const int chunk = b % p.nchunk;
+    const int n = b / p.nchunk;
+    const int c0 = chunk * p.CB;
+    const int p0 = band * p.PB;
+    const int pend = min(p0 + p.PB, p.P);
+    const int row0 = p0 * p.sh - p.ph;  // first input row of the band (may be < 0)
+    const int HW = p.H * p.W;
+    const int plane = p.RB * p.W;
+
+    // 1. stage the input: element e = (j, r, w), channel c0 - HALF + j, row row0 + r
+    const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(p.x + (size_t)n * p.C * HW), (short)0, 0x7fffffff, 0x00020000);
+    const int nin = CIN * plane;
+    constexpr int kBurst = 32;
+    for (int e0 = threadIdx.x; e0 < nin; e0 += kBurst * kThreads) {
+        float v[kBurst];
+#pragma unroll
+        for (int u = 0; u < kBurst; ++u) {
+            const int e = e0 + u * kThreads;
+            const int j = (int)fdiv(e, p.f_plane);
+            const int rw = e - j * plane;
+            const int r = (int)fdiv(rw, p.f_w);
+            const int w = rw - r * p.W;
+            const int c = c0 - HALF + j;
+            const int h = row0 + r;
+            const bool ok = e < nin && (unsigned)c < (unsigned)p.C && (unsigned)h < (unsigned)p.H;
+            const int off = ok ? (c * HW + h * p.W + w) * 4 : (int)0x80000000u;
+            v[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0));
+        }
+#pragma unroll
+        for (int u = 0; u < kBurst; ++u)
+            if (e0 + u * kThreads < nin) in[e0 + u * kThreads] = v[u];
+    }
+    __syncthreads();
+
+    // 2. LRN of the CB channels over the band, in place: channel c's value
+    //    goes to staged channel c + HALF, read into the window at step c - HALF
+    for (int rw = threadIdx.x; rw < plane; rw += kThreads) {
+        float win[WIN];
+#pragma unroll
+        for (int j = 0; j < WIN - 1; ++j) win[j] = in[j * plane + rw];
+        for (int c = 0; c < p.CB; ++c) {
+            win[WIN - 1] = in[(c + WIN - 1) * plane + rw];
+            const float v = lrn_value<WIN>(win, p.k, p.alpha_over_size, p.beta);
+            in[(c + HALF) * plane + rw] = v;
+#pragma unroll
+            for (int j = 0; j < WIN - 1; ++j) win[j] = win[j + 1];
+        }
+    }
+    __syncthreads();
+    const float* lrn = in + HALF * plane;  // [CB][RB][W]
+
+    // 3. pooling from the LRN tile
+    const int PQ = p.P * p.Q;
+    const int pbq = p.PB * p.Q;
+    const int nout = p.CB * pbq;
+    for (int o = threadIdx.x; o < nout; o += kThreads) {
+        const int c = (int)fdiv(o, p.f_pbq);
+        const int rq = o - c * pbq;
+        const int pr = (int)fdiv(rq, p.f_q);
+        const int q = rq - pr * p.Q;
+        const int pp = p0 + pr;
+        if (c0 + c >= p.C || pp >= pend) continue;
+        const int hs = pp * p.sh - p.ph, ws = q * p.sw - p.pw;
+        const int h0 = max(hs, 0), w0 = max(ws, 0);
+        const int h1 = min(hs + p.kh, p.H), w1 = min(ws + p.kw, p.W);
+        const float* t = lrn + c * plane;
+        float out;
+        if constexpr (MODE == 0) {
+            int bi = h0 * p.W + w0;  // first maximum in row-major order
+            float best = t[(h0 - row0) * p.W + w0];
+            for (int h = h0; h < h1; ++h)
+                for (int w = w0; w < w1; ++w) {
+                    const float v = t[(h - row0) * p.W + w];
+                    if (v > best) {
+                        best = v;
+                        bi = h * p.W + w;
+                    }
+                }
+            out = best;
+            if (WITH_IDX) p.idx[(size_t)(n * p.C + c0 + c) * PQ + pp * p.Q + q] = bi;
+        } else {
+            const int count = (min(hs + p.kh, p.H + p.ph) - hs) * (min(ws + p.kw, p.W + p.pw) - ws);
+            float sum = 0.0f;
+            for (int h = h0; h < h1; ++h)
+                for (int w = w0; w < w1; ++w) sum += t[(h - row0) * p.W + w];
+            out = sum / (float)count;
+        }
+        if (p.relu) out = out > 0.0f ? out : 0.0f;
+        p.y[(size_t)(n * p.C + c0 + c) * PQ + pp * p.Q + q] = out;
     }
 }
 
@@ -354,6 +491,90 @@ int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha
         if (rc != CNN_OK) return rc;
     }
     return CNN_OK;
+}
+
+namespace {
+constexpr int kLrnPoolLds = 32 * 1024;  // LDS budget of one fused workgroup (4+ per CU)
+
+// Channels and output rows per workgroup of the fused LRN + pooling kernel:
+// among the tilings that fit the LDS budget, the one that reads the fewest
+// input elements per output (channel halo and overlapping band rows are read
+// twice); false when none fits.
+bool lrn_pool_tiling(const PoolShape& s, int half, int* CB, int* PB, int* RB) {
+    double best = 1e30;
+    for (int cb : {32, 16, 8, 4}) {
+        if (cb > 4 && cb / 2 >= s.C) continue;  // no wider than the channels need
+        for (int pb = std::min(s.P, 16); pb >= 1; --pb) {
+            const int rb = (pb - 1) * s.sh + s.kh;
+            const int64_t bytes = (int64_t)(cb + 2 * half) * rb * s.W * 4;
+            if (bytes > kLrnPoolLds) continue;
+            const double cost = (double)(cb + 2 * half) * rb / ((double)std::min(cb, s.C) * pb);
+            if (cost < best - 1e-9) {
+                best = cost;
+                *CB = cb;
+                *PB = pb;
+                *RB = rb;
+            }
+            break;  // the tallest band that fits is the cheapest for this cb
+        }
+    }
+    return best < 1e29;
+}
+}  // namespace
+
+bool lrn_pool_fusable(const PoolShape& s, int size) {
+    int cb, pb, rb;
+    if (size % 2 != 1 || size / 2 > 4 || (int64_t)s.C * s.H * s.W >= ((int64_t)1 << 29) ||
+        !lrn_pool_tiling(s, size / 2, &cb, &pb, &rb))
+        return false;
+    // the launch's work-items fit 32 bits
+    const int64_t blocks = (int64_t)s.N * ceil_div(s.C, cb) * ceil_div(s.P, pb);
+    return blocks * kThreads < ((int64_t)1 << 32);
+}
+
+int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alpha, float beta, float k,
+                    const float* x, float* y, int32_t* idx, hipStream_t st) {
+    if (s.N == 0) return CNN_OK;
+    const int half = size / 2;
+    LrnPoolParams p;
+    if (!lrn_pool_fusable(s, size) || !lrn_pool_tiling(s, half, &p.CB, &p.PB, &p.RB))
+        return fail(CNN_ERR_UNSUPPORTED, "lrn+pool: no fused tiling for this shape");
+    p.x = x;
+    p.y = y;
+    p.idx = idx;
+    p.C = s.C; p.H = s.H; p.W = s.W; p.P = s.P; p.Q = s.Q;
+    p.kh = s.kh; p.kw = s.kw; p.sh = s.sh; p.sw = s.sw; p.ph = s.ph; p.pw = s.pw;
+    p.nchunk = ceil_div(s.C, p.CB);
+    p.nband = ceil_div(s.P, p.PB);
+    p.f_plane = make_fastdiv(p.RB * s.W);
+    p.f_w = make_fastdiv(s.W);
+    p.f_pbq = make_fastdiv(p.PB * s.Q);
+    p.f_q = make_fastdiv(s.Q);
+    p.relu = relu;
+    p.alpha_over_size = alpha / (float)size;
+    p.beta = beta;
+    p.k = k;
+    const int64_t blocks = (int64_t)s.N * p.nchunk * p.nband;
+    const size_t shm = (size_t)(p.CB + 2 * half) * p.RB * s.W * 4;
+    const dim3 grid((unsigned)blocks), block(kThreads);
+#define CNN_LRN_POOL(H)                                                                          \
+    do {                                                                                         \
+        if (mode == CNN_POOL_MAX && idx)                                                         \
+            hipLaunchKernelGGL((lrn_pool_f32<H, 0, true>), grid, block, shm, st, p);             \
+        else if (mode == CNN_POOL_MAX)                                                           \
+            hipLaunchKernelGGL((lrn_pool_f32<H, 0, false>), grid, block, shm, st, p);            \
+        else                                                                                     \
+            hipLaunchKernelGGL((lrn_pool_f32<H, 1, false>), grid, block, shm, st, p);            \
+    } while (0)
+    switch (half) {
+        case 0: CNN_LRN_POOL(0); break;
+        case 1: CNN_LRN_POOL(1); break;
+        case 2: CNN_LRN_POOL(2); break;
+        case 3: CNN_LRN_POOL(3); break;
+        default: CNN_LRN_POOL(4); break;
+    }
+#undef CNN_LRN_POOL
+    return check_launch("lrn_pool_f32");
 }
 
 int launch_relu(const float* x, float* y, int64_t n, hipStream_t st) {

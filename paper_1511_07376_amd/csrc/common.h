@@ -72,6 +72,12 @@ int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y
 int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha, float beta,
                float k, float* y, hipStream_t st);
 int launch_relu(const float* x, float* y, int64_t n, hipStream_t st);
+// LRN (across channels, odd size) followed by pooling of its output, in one
+// kernel; s is the pooling shape (its input is the LRN's shape).  Only where
+// lrn_pool_fusable() holds.
+bool lrn_pool_fusable(const PoolShape& s, int size);
+int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alpha, float beta, float k,
+                    const float* x, float* y, int32_t* idx, hipStream_t st);
 int launch_softmax(const float* x, int N, int C, int HW, float* y, hipStream_t st);
 
 }  // namespace cnn
