@@ -32,16 +32,19 @@ PEAK_HBM_GBS = 8000.0           # MI355X HBM3E
 
 
 def layer_work(net, batch, cnn):
-    """Per layer: (name, kind, flops, bytes, kernel) with algorithmic counts.
+    """Per layer: (name, kind, flops, bytes) with algorithmic counts.
 
     conv: 2*N*K*P*Q*(C/G)*R*S flops; fc: 2*N*I*O flops; pool: read input +
     write output (+ int32 index); LRN: read + write; ReLU: read + write.
     Bytes are fp32 tensor sizes; parameters are counted for conv / fc only as
-    part of the contraction, not as bandwidth."""
+    part of the contraction, not as bandwidth.  An LRN layer followed by a
+    pooling layer runs inside the pooling kernel: the LRN gets kind "fused"
+    and no bytes, the pooling layer the LRN's read and its own write."""
     c, h, w = net.input_chw
     out = []
     counts = {}
-    for layer in net.layers:
+    layers = list(net.layers)
+    for li, layer in enumerate(layers):
         counts[layer.kind] = counts.get(layer.kind, 0) + 1
         name = f"{layer.kind}{counts[layer.kind]}"
         if layer.kind == "conv":
@@ -58,10 +61,12 @@ def layer_work(net, batch, cnn):
         elif layer.kind == "pool":
             p, q = cnn.cnn_pool_out_shape(h, w, layer.kernel, layer.stride, layer.pad, layer.ceil)
             byts = 4 * batch * c * (h * w + p * q)
-            out.append((name, "pool", 0, byts))
+            kind = "lrn+pool" if li > 0 and layers[li - 1].kind == "lrn" else "pool"
+            out.append((name, kind, 0, byts))
             h, w = p, q
         elif layer.kind == "lrn":
-            out.append((name, "lrn", 0, 8 * batch * c * h * w))
+            fused = li + 1 < len(layers) and layers[li + 1].kind == "pool"
+            out.append((name, "fused" if fused else "lrn", 0, 0 if fused else 8 * batch * c * h * w))
         elif layer.kind == "softmax":
             out.append((name, "softmax", 0, 8 * batch * c * h * w))
         else:
@@ -238,6 +243,8 @@ def main():
             tf = flops / (ms * 1e-3) / 1e12 if ms > 0 else 0.0
             ent.update({"gflop": round(flops / 1e9, 4), "tflops": round(tf, 2),
                         "frac_fp32_mfma": round(tf / PEAK_FP32_MFMA_TFLOPS, 4)})
+        elif kind == "fused":
+            ent["runs_inside_next_layer"] = True  # the interval holds only the event records
         else:
             gbs = byts / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
             ent.update({"mbytes": round(byts / 1e6, 2), "gbs": round(gbs, 1),
