@@ -252,8 +252,8 @@ FcGeom fc_geom(int N) {
 // Splits and the reduction length per split.
 int fc_split(const FcGeom& g, int N, int I, int O, int* kchunk) {
     const int tiles = ceil_div(N, g.tm) * ceil_div(O, g.tn);
-    // enough splits to reach the target, but at least two rounds per split
-    int splits = std::min(ceil_div(g.target, tiles), std::max(1, I / (2 * g.unit)));
+    // enough splits to reach the target, but at least one round per split
+    int splits = std::min(ceil_div(g.target, tiles), std::max(1, I / g.unit));
     splits = std::max(splits, 1);
     *kchunk = ceil_div(ceil_div(I, splits), g.unit) * g.unit;
     return ceil_div(I, *kchunk);
