@@ -17,11 +17,12 @@
 // branches.
 //
 // Workgroup tile: TM output channels x TN output pixels, reduction in slabs of
-// BK taps, double-buffered in LDS, with the loads of slabs s+1 and s+2 in
-// flight in two register stages while slab s feeds the matrix cores.  Each wave owns FM x FN blocks of 32x32
-// accumulated with v_mfma_f32_32x32x2_f32.  The output channel is the MFMA
-// row and the output pixel the MFMA column, so the 32 lanes of a row store 32
-// consecutive pixels: NCHW stores are coalesced.
+// BK taps, double-buffered in LDS, with the loads of the next ST slabs in
+// flight in ST register stages while slab s feeds the matrix cores.  Each
+// wave owns FM x FN blocks of 32x32 accumulated with v_mfma_f32_32x32x2_f32.
+// The output channel is the MFMA row and the output pixel the MFMA column,
+// so the 32 lanes of a row store 32 consecutive pixels: NCHW stores are
+// coalesced.
 //
 // Reduction order inside a slab: lanes 0-31 take the first BK/2 taps of the
 // slab and lanes 32-63 the last BK/2 (an MFMA step consumes one tap per lane
