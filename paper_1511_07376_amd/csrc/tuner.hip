@@ -10,12 +10,14 @@
 // buffers and stream, times each with HIP events, and records the fastest;
 // later calls of that shape use it.  The table can be exported as text and
 // imported again, so the search runs once per machine.
+#include <algorithm>
 #include <cstdio>
 #include <cstring>
 #include <map>
 #include <mutex>
 #include <string>
 #include <tuple>
+#include <vector>
 
 #include "common.h"
 
@@ -32,9 +34,15 @@ std::mutex g_mu;
 std::map<Key, int> g_table;  // shape -> configuration index
 int g_autotune = 0;
 
-constexpr int kTimedRuns = 3;
+constexpr int kTimedRuns = 3;   // first pass, every configuration
+constexpr int kFinalists = 3;   // re-timed ...
+constexpr int kFinalRuns = 5;   // ... this many runs per round ...
+constexpr int kFinalRounds = 2; // ... in interleaved rounds, keeping each one's best
 
 // Times every configuration on this shape; returns the fastest, or -1.
+// Configurations a few percent apart can swap places from one timing to the
+// next, so the fastest few of the first pass are timed again, interleaved,
+// and each keeps its best round.
 int tune(const ConvShape& s, const float* x, const float* w, const float* bias, int relu, float* y,
          hipStream_t st) {
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
@@ -45,21 +53,37 @@ int tune(const ConvShape& s, const float* x, const float* w, const float* bias, 
         hipEventDestroy(e0);
         return -1;
     }
-    int best = -1;
-    float best_ms = 0.0f;
-    for (int c = 0; c < conv2d_num_configs(); ++c) {
-        if (launch_conv2d(s, x, w, bias, relu, y, st, c) != CNN_OK) continue;  // warm-up run
+    // ms per run of configuration c over `runs` back-to-back launches; < 0 on failure
+    auto time_cfg = [&](int c, int runs) -> float {
+        if (launch_conv2d(s, x, w, bias, relu, y, st, c) != CNN_OK) return -1.0f;  // warm-up run
         hipEventRecord(e0, st);
-        for (int r = 0; r < kTimedRuns; ++r) launch_conv2d(s, x, w, bias, relu, y, st, c);
+        for (int r = 0; r < runs; ++r) launch_conv2d(s, x, w, bias, relu, y, st, c);
         hipEventRecord(e1, st);
-        if (hipEventSynchronize(e1) != hipSuccess) break;
+        if (hipEventSynchronize(e1) != hipSuccess) return -1.0f;
         float ms = 0.0f;
-        if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) continue;
-        if (best < 0 || ms < best_ms) {
-            best = c;
-            best_ms = ms;
-        }
+        if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) return -1.0f;
+        return ms / runs;
+    };
+    std::vector<std::pair<float, int>> first;
+    for (int c = 0; c < conv2d_num_configs(); ++c) {
+        const float ms = time_cfg(c, kTimedRuns);
+        if (ms >= 0.0f) first.emplace_back(ms, c);
     }
+    std::sort(first.begin(), first.end());
+    const int nf = std::min<int>(kFinalists, (int)first.size());
+    std::vector<float> best_ms(nf, 1e30f);
+    for (int round = 0; round < kFinalRounds; ++round)
+        for (int i = 0; i < nf; ++i) {
+            const float ms = time_cfg(first[i].second, kFinalRuns);
+            if (ms >= 0.0f) best_ms[i] = std::min(best_ms[i], ms);
+        }
+    int best = nf > 0 ? first[0].second : -1;
+    float top = 1e30f;
+    for (int i = 0; i < nf; ++i)
+        if (best_ms[i] < top) {
+            top = best_ms[i];
+            best = first[i].second;
+        }
     hipEventDestroy(e0);
     hipEventDestroy(e1);
     (void)hipGetLastError();
