@@ -210,9 +210,10 @@ int cnn_net_out_shape(const cnn_layer_desc* layers, int n_layers, int N, int C,
 
 /* Device workspace cnn_net_fwd needs for this input: two activation buffers
  * of the largest intermediate tensor, each 256-byte aligned, plus room for
- * the outputs of the FC layers whose reduction is split across workgroups
- * (they are set to their biases together at the start of a pass).  0 on
- * error. */
+ * the outputs of the conv and FC layers whose reduction may be split across
+ * workgroups (small outputs, e.g. at batch 1; they are set to their biases
+ * together at the start of a pass).  The size does not depend on tuning.
+ * 0 on error. */
 size_t cnn_net_workspace_bytes(const cnn_layer_desc* layers, int n_layers,
                                int N, int C, int H, int W);
 

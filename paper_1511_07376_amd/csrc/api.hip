@@ -139,9 +139,12 @@ struct Plan {
     bool skipped;          // a RELU layer folded into its predecessor, or an LRN
                            // layer run inside the pooling layer after it
     int lrn_from;          // POOL: index of the LRN layer it runs first, or -1
-    bool fc_split;         // FC: the reduction is split (output must start as the bias)
-    size_t fc_off;         // FC with fc_split, not last: byte offset of its output in
-                           // the FC area of the workspace
+    bool may_split;        // CONV, FC: some configuration splits the reduction
+                           // across workgroups (room is kept for the output)
+    bool split;            // ... and the one the launch will use does (the
+                           // output must start as the bias)
+    size_t split_off;      // may_split, not last: byte offset of its output in
+                           // the split-output area of the workspace
     ConvShape conv;
     PoolShape pool;
 };
@@ -150,11 +153,12 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 // need_weights: the net is about to run (shape queries take descriptors
-// without parameters).  *fc_bytes: size of the workspace area that holds the
-// outputs of split-reduction FC layers (other than the last layer), which
-// are all set to their biases by one launch at the start of the pass.
+// without parameters).  *split_bytes: size of the workspace area that holds
+// the outputs of split-reduction conv and FC layers (other than the last
+// layer), which are all set to their biases by one launch at the start of
+// the pass.
 int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* plan,
-             int64_t* max_elems, bool need_weights = true, size_t* fc_bytes = nullptr) {
+             int64_t* max_elems, bool need_weights = true, size_t* split_bytes = nullptr) {
     if (!L || n <= 0) return fail(CNN_ERR_INVALID, "net: no layers");
     if (N < 0 || C <= 0 || H <= 0 || W <= 0)
         return fail(CNN_ERR_INVALID, "net: input %dx%dx%dx%d", N, C, H, W);
@@ -181,6 +185,17 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
                 if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
                 c = d.out_channels; h = p.conv.P; w = p.conv.Q;
                 p.relu = d.fuse_relu != 0;
+                if (N > 0) {
+                    // the workspace does not depend on tuning: room for the output of
+                    // any conv that some configuration splits; used when the
+                    // configuration the launch will use (known unless it is still to
+                    // be tuned) splits
+                    for (int cfg = 0; cfg < conv2d_num_configs() && !p.may_split; ++cfg)
+                        p.may_split = conv2d_splits(p.conv, cfg) > 1;
+                    const int cfg = conv2d_planned_config(p.conv);
+                    p.split = cfg != -2 && conv2d_splits(p.conv, cfg) > 1;
+                    p.may_split = p.may_split || p.split;
+                }
                 break;
             }
             case CNN_LAYER_FC: {
@@ -193,7 +208,7 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
                 if (I > kMaxElems) return fail(CNN_ERR_UNSUPPORTED, "net layer %d: fc input too large", i);
                 rc = check_fc(N, (int)I, d.out_channels);
                 if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
-                p.fc_split = fc_splits(N, (int)I, d.out_channels) > 1;
+                p.split = p.may_split = fc_splits(N, (int)I, d.out_channels) > 1;
                 c = d.out_channels; h = 1; w = 1;
                 p.relu = d.fuse_relu != 0;
                 break;
@@ -243,14 +258,15 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
     *max_elems = mx;
     int last = n - 1;
     while (last > 0 && plan[last].skipped) --last;
-    size_t fc = 0;
+    size_t area = 0;
     for (int i = 0; i < n; ++i) {
-        if (plan[i].type == CNN_LAYER_FC && plan[i].fc_split && i != last) {
-            plan[i].fc_off = fc;
-            fc += align_up((size_t)N * plan[i].outC * sizeof(float));
+        Plan& p = plan[i];
+        if (p.may_split && !p.skipped && i != last) {
+            p.split_off = area;
+            area += align_up((size_t)N * p.outC * p.outH * p.outW * sizeof(float));
         }
     }
-    if (fc_bytes) *fc_bytes = fc;
+    if (split_bytes) *split_bytes = area;
     return CNN_OK;
 }
 
@@ -260,8 +276,8 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
     if (n > 4096) return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n);
     std::vector<Plan> plan((size_t)std::max(n, 0));
     int64_t mx = 0;
-    size_t fc_bytes = 0;
-    int rc = plan_net(L, n, N, C, H, W, plan.data(), &mx, true, &fc_bytes);
+    size_t split_bytes = 0;
+    int rc = plan_net(L, n, N, C, H, W, plan.data(), &mx, true, &split_bytes);
     if (rc) return rc;
     if (N == 0) {  // nothing to compute; still honour the event contract
         for (int i = 0; events && i <= n; ++i)
@@ -270,34 +286,34 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
         return CNN_OK;
     }
     const size_t half = align_up((size_t)mx * sizeof(float));
-    if (!ws || ws_bytes < 2 * half + fc_bytes)
+    if (!ws || ws_bytes < 2 * half + split_bytes)
         return fail(CNN_ERR_WORKSPACE, "net: workspace of %zu bytes, %zu needed", ws_bytes,
-                    2 * half + fc_bytes);
+                    2 * half + split_bytes);
     if (reinterpret_cast<uintptr_t>(ws) % 16)
         return fail(CNN_ERR_INVALID, "net: workspace must be 16-byte aligned");
     float* buf[2] = {static_cast<float*>(ws),
                      reinterpret_cast<float*>(static_cast<char*>(ws) + half)};
-    char* fc_area = static_cast<char*>(ws) + 2 * half;
+    char* split_area = static_cast<char*>(ws) + 2 * half;
 
     int last = n - 1;
     while (last > 0 && plan[last].skipped) --last;
 
-    // Every split-reduction FC output starts as its bias: one launch for all.
+    // Every split-reduction output starts as its bias: one launch for all.
     {
-        std::vector<FcFill> fills;
+        std::vector<BiasFill> fills;
         for (int i = 0; i < n; ++i) {
             const Plan& p = plan[i];
-            if (p.type != CNN_LAYER_FC || !p.fc_split) continue;
-            float* dst = i == last ? y : reinterpret_cast<float*>(fc_area + p.fc_off);
-            fills.push_back(FcFill{dst, L[i].bias, N, p.outC});
+            if (!p.split || p.skipped) continue;
+            float* dst = i == last ? y : reinterpret_cast<float*>(split_area + p.split_off);
+            fills.push_back(BiasFill{dst, L[i].bias, N, p.outC, p.outH * p.outW});
         }
-        rc = launch_fc_fills(fills.data(), (int)fills.size(), st);
+        rc = launch_bias_fills(fills.data(), (int)fills.size(), st);
         if (rc) return rc;
     }
 
     const float* cur = x;
     int next_buf = 0;
-    bool relu_pending = false;  // cur still needs the previous FC layer's ReLU
+    bool relu_pending = false;  // cur still needs the previous layer's ReLU
     for (int i = 0; i < n; ++i) {
         if (events) {
             if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), st) != hipSuccess)
@@ -307,39 +323,45 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
         if (p.skipped) continue;
         const cnn_layer_desc& d = L[i];
         float* out = (i == last) ? y : buf[next_buf];
-        if (p.type == CNN_LAYER_FC && p.fc_split && i != last)
-            out = reinterpret_cast<float*>(fc_area + p.fc_off);
+        if (p.split && i != last) out = reinterpret_cast<float*>(split_area + p.split_off);
+        // A ReLU that a split-reduction layer would run as a pass of its own is
+        // left to the next layer when that layer can take its input through a
+        // ReLU as it reads it (conv, FC, pooling, LRN).
+        int nx = i + 1;
+        while (nx < n && plan[nx].skipped) ++nx;
+        const bool next_takes_relu = nx < n && (plan[nx].type == CNN_LAYER_CONV || plan[nx].type == CNN_LAYER_FC ||
+                                                plan[nx].type == CNN_LAYER_POOL || plan[nx].type == CNN_LAYER_LRN);
+        bool* relu_left = next_takes_relu ? &relu_pending : nullptr;
+        const bool relu_in = relu_pending;
+        relu_pending = false;
         // an in-place ReLU or softmax keeps its buffer
         if ((p.type == CNN_LAYER_RELU || p.type == CNN_LAYER_SOFTMAX) && i != last && cur != x)
             out = const_cast<float*>(cur);
         switch (p.type) {
-            case CNN_LAYER_CONV:
-                rc = conv2d_dispatch(p.conv, cur, d.weight, d.bias, p.relu, out, st);
-                break;
-            case CNN_LAYER_FC: {
-                // A ReLU after a split-reduction FC layer whose output only feeds
-                // another FC layer is applied as that layer reads its input.
-                int nx = i + 1;
-                while (nx < n && plan[nx].skipped) ++nx;
-                const bool next_fc = nx < n && plan[nx].type == CNN_LAYER_FC;
-                const bool relu_in = relu_pending;
-                relu_pending = false;
-                rc = launch_fc(cur, N, p.inC * p.inH * p.inW, d.weight, d.bias, p.outC, p.relu, out, st,
-                               relu_in, next_fc ? &relu_pending : nullptr, p.fc_split);
+            case CNN_LAYER_CONV: {
+                ConvOpts o;
+                o.relu_in = relu_in;
+                o.prefilled = p.split;
+                o.relu_left = relu_left;
+                rc = conv2d_dispatch(p.conv, cur, d.weight, d.bias, p.relu, out, st, &o);
                 break;
             }
+            case CNN_LAYER_FC:
+                rc = launch_fc(cur, N, p.inC * p.inH * p.inW, d.weight, d.bias, p.outC, p.relu, out, st,
+                               relu_in, relu_left, p.split);
+                break;
             case CNN_LAYER_POOL:
                 if (p.lrn_from >= 0) {  // cur is still the LRN's input
                     const cnn_layer_desc& ld = L[p.lrn_from];
                     rc = launch_lrn_pool(p.pool, d.pool_mode, p.relu, ld.lrn_size, ld.lrn_alpha,
-                                         ld.lrn_beta, ld.lrn_k, cur, out, d.pool_index, st);
+                                         ld.lrn_beta, ld.lrn_k, cur, out, d.pool_index, st, relu_in);
                 } else {
-                    rc = launch_pool(p.pool, d.pool_mode, p.relu, cur, out, d.pool_index, st);
+                    rc = launch_pool(p.pool, d.pool_mode, p.relu, cur, out, d.pool_index, st, relu_in);
                 }
                 break;
             case CNN_LAYER_LRN:
                 rc = launch_lrn(cur, N, p.inC, p.inH, p.inW, d.lrn_size, d.lrn_alpha, d.lrn_beta,
-                                d.lrn_k, out, st);
+                                d.lrn_k, out, st, relu_in);
                 break;
             case CNN_LAYER_RELU:
                 rc = launch_relu(cur, out, (int64_t)N * p.inC * p.inH * p.inW, st);
@@ -464,9 +486,9 @@ size_t cnn_net_workspace_bytes(const cnn_layer_desc* layers, int n_layers, int N
     if (n_layers > 4096 || n_layers <= 0) return 0;
     std::vector<Plan> plan((size_t)n_layers);
     int64_t mx;
-    size_t fc_bytes = 0;
-    if (plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx, false, &fc_bytes)) return 0;
-    return 2 * align_up((size_t)mx * sizeof(float)) + fc_bytes;
+    size_t split_bytes = 0;
+    if (plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx, false, &split_bytes)) return 0;
+    return 2 * align_up((size_t)mx * sizeof(float)) + split_bytes;
 }
 
 int cnn_net_fwd(const cnn_layer_desc* layers, int n_layers, const float* x, int N, int C, int H,

@@ -19,6 +19,10 @@ inline int grid_for(int64_t items, int per_thread = 1) {
 // ------------------------------------------------------------------ pooling
 // One thread per output element, lanes along the output row, so the lanes of
 // a wave read neighbouring windows of the same input rows.
+// v, or max(v, 0) when on: the input of a layer whose producer left its
+// ReLU to it (the network executor does so after a split reduction).
+__device__ inline float relu_in(float v, int on) { return on ? (v > 0.0f ? v : 0.0f) : v; }
+
 struct PoolParams {
     const float* x;
     float* y;
@@ -26,6 +30,7 @@ struct PoolParams {
     int H, W, P, Q, kh, kw, sh, sw, ph, pw;
     int total;  // N*C*P*Q
     int relu;
+    int relu_x;  // take the input through a ReLU as it is read
 };
 
 template <bool WITH_IDX>
@@ -41,11 +46,11 @@ __global__ void __launch_bounds__(kThreads) maxpool_f32(PoolParams p) {
         const int h1 = min(hs + p.kh, p.H), w1 = min(ws + p.kw, p.W);
         // first maximum in row-major order: strict comparison
         int bi = h0 * p.W + w0;
-        float best = plane[bi];
+        float best = relu_in(plane[bi], p.relu_x);
         for (int h = h0; h < h1; ++h) {
             const float* row = plane + h * p.W;
             for (int w = w0; w < w1; ++w) {
-                const float v = row[w];
+                const float v = relu_in(row[w], p.relu_x);
                 if (v > best) {
                     best = v;
                     bi = h * p.W + w;
@@ -102,7 +107,7 @@ pool_staged_f32(PoolParams p, int planes_per_block, int nplanes, FastDiv fpq, Fa
 #pragma unroll
             for (int u = 0; u < 16; ++u) {
                 const int i = threadIdx.x + u * kThreads;
-                if (i < len) tile[i] = v[u];
+                if (i < len) tile[i] = relu_in(v[u], p.relu_x);
             }
         }
         __syncthreads();
@@ -159,7 +164,7 @@ __global__ void __launch_bounds__(kThreads) avgpool_f32(PoolParams p) {
         float sum = 0.0f;
         for (int h = h0; h < h1; ++h) {
             const float* row = plane + h * p.W;
-            for (int w = w0; w < w1; ++w) sum += row[w];
+            for (int w = w0; w < w1; ++w) sum += relu_in(row[w], p.relu_x);
         }
         float v = sum / (float)count;
         if (p.relu) v = v > 0.0f ? v : 0.0f;
@@ -181,6 +186,7 @@ struct LrnParams {
     int nchunk;  // ceil(C / CCH)
     int total;   // N * nchunk * H*W
     float alpha_over_size, beta, k;
+    int relu_x;  // take the input through a ReLU as it is read
 };
 
 // scale^(-beta) through the hardware base-2 logarithm and exponential
@@ -223,7 +229,8 @@ __global__ void __launch_bounds__(kThreads) lrn_across_f32(LrnParams p) {
         for (int j = 0; j < NV; ++j) {
             const int cc = c0 - HALF + j;
             const int off = (unsigned)cc < (unsigned)p.C ? (base + cc * p.HW) * 4 : (int)0x80000000u;
-            v[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0));
+            v[j] = relu_in(__builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0)),
+                           p.relu_x);
         }
         float* yp = p.y + base;
 #pragma unroll
@@ -254,6 +261,7 @@ struct LrnPoolParams {
     int C, H, W, P, Q, kh, kw, sh, sw, ph, pw;
     int CB, PB, RB;   // channels, output rows and input rows per workgroup
     int nchunk, nband;
+    int relu_x;       // take the input through a ReLU as it is read
     FastDiv f_plane, f_w, f_pbq, f_q;  // RB*W, W, PB*Q, Q
     int relu;
     float alpha_over_size, beta, k;
@@ -298,7 +306,7 @@ __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
         }
 #pragma unroll
         for (int u = 0; u < kBurst; ++u)
-            if (e0 + u * kThreads < nin) in[e0 + u * kThreads] = v[u];
+            if (e0 + u * kThreads < nin) in[e0 + u * kThreads] = relu_in(v[u], p.relu_x);
     }
     __syncthreads();
 
@@ -371,11 +379,11 @@ __global__ void __launch_bounds__(kThreads) lrn_across_any_f32(LrnParams p, int 
             const int c0 = max(c - half, 0), c1 = min(c + half, p.C - 1);
             float sq = 0.0f;
             for (int cc = c0; cc <= c1; ++cc) {
-                const float v = xp[cc * p.HW];
+                const float v = relu_in(xp[cc * p.HW], p.relu_x);
                 sq += v * v;
             }
             const float scale = p.k + p.alpha_over_size * sq;
-            yp[c * p.HW] = xp[c * p.HW] * pow_neg(scale, p.beta);
+            yp[c * p.HW] = relu_in(xp[c * p.HW], p.relu_x) * pow_neg(scale, p.beta);
         }
     }
 }
@@ -400,8 +408,9 @@ __global__ void __launch_bounds__(kThreads) relu_f32(const float* x, float* y, i
 }  // namespace
 
 int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y, int32_t* idx,
-                hipStream_t st) {
+                hipStream_t st, bool relu_x) {
     PoolParams p;
+    p.relu_x = relu_x;
     p.x = x;
     p.y = y;
     p.idx = idx;
@@ -451,8 +460,9 @@ int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y
 }
 
 int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha, float beta,
-               float k, float* y, hipStream_t st) {
+               float k, float* y, hipStream_t st, bool relu_x) {
     LrnParams p;
+    p.relu_x = relu_x;
     p.x = x;
     p.y = y;
     p.C = C;
@@ -533,7 +543,7 @@ bool lrn_pool_fusable(const PoolShape& s, int size) {
 }
 
 int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alpha, float beta, float k,
-                    const float* x, float* y, int32_t* idx, hipStream_t st) {
+                    const float* x, float* y, int32_t* idx, hipStream_t st, bool relu_x) {
     if (s.N == 0) return CNN_OK;
     const int half = size / 2;
     LrnPoolParams p;
@@ -554,6 +564,7 @@ int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alph
     p.alpha_over_size = alpha / (float)size;
     p.beta = beta;
     p.k = k;
+    p.relu_x = relu_x;
     const int64_t blocks = (int64_t)s.N * p.nchunk * p.nband;
     const size_t shm = (size_t)(p.CB + 2 * half) * p.RB * s.W * 4;
     const dim3 grid((unsigned)blocks), block(kThreads);

@@ -38,46 +38,64 @@ int pool_out(int H, int W, int kh, int kw, int sh, int sw, int ph, int pw, int c
 
 // Launchers: arguments already validated; they enqueue and return CNN_OK or
 // CNN_ERR_HIP.
+// Options of a convolution run inside a network:
+//   relu_in   take the input through a ReLU as it is read (the producer left
+//             its ReLU to this layer);
+//   prefilled y already holds the bias (only with a split reduction);
+//   relu_left non-null: a ReLU that would need a pass of its own (split
+//             reduction) is skipped and *relu_left set, for the consumer.
+struct ConvOpts {
+    bool relu_in = false;
+    bool prefilled = false;
+    bool* relu_left = nullptr;
+};
 // cfg: index into the convolution configuration table, or -1 for the
 // built-in heuristic.
 int launch_conv2d(const ConvShape& s, const float* x, const float* w, const float* bias,
-                  int relu, float* y, hipStream_t st, int cfg);
+                  int relu, float* y, hipStream_t st, int cfg, const ConvOpts* opt = nullptr);
 int conv2d_num_configs();
 const char* conv2d_config_name(int i);
+// Reduction splits configuration cfg (-1: heuristic) uses for this shape.
+int conv2d_splits(const ConvShape& s, int cfg);
 // Convolution with the tuned configuration for this shape (auto-tuning it
 // first when auto-tuning is on and the shape is new).
 int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const float* bias,
-                    int relu, float* y, hipStream_t st);
+                    int relu, float* y, hipStream_t st, const ConvOpts* opt = nullptr);
+// The configuration conv2d_dispatch would use now: the tuned one, else the
+// heuristic (-1); -2 when the shape would be auto-tuned first.
+int conv2d_planned_config(const ConvShape& s);
 // relu_in: apply a ReLU to x as it is read.  relu_left non-null: when the
 // layer's ReLU would need a pass of its own (split reduction), skip it and set
 // *relu_left, so that the caller can fold it into the next layer's input.
-// prefilled: y already holds the bias (see fc_splits, launch_fc_fills).
+// prefilled: y already holds the bias (see fc_splits, launch_bias_fills).
 int launch_fc(const float* x, int N, int I, const float* w, const float* bias, int O, int relu,
               float* y, hipStream_t st, bool relu_in = false, bool* relu_left = nullptr,
               bool prefilled = false);
 // Reduction splits launch_fc uses for this shape; above 1 its output must
 // start as the bias (launch_fc fills it unless told it is prefilled).
 int fc_splits(int N, int I, int O);
-// y_j[n][o] = bias_j[o] (or 0) for several FC outputs, in one launch per
-// kMaxFcFills jobs.
-constexpr int kMaxFcFills = 8;
-struct FcFill {
+// y_j[n][o][i] = bias_j[o] (or 0), i < inner, for several layer outputs
+// (FC: inner = 1; conv NCHW: inner = P*Q), in one launch per kMaxBiasFills
+// jobs.
+constexpr int kMaxBiasFills = 8;
+struct BiasFill {
     float* y;
     const float* bias;
-    int N, O;
+    int N, O, inner;
 };
-int launch_fc_fills(const FcFill* jobs, int n, hipStream_t st);
+int launch_bias_fills(const BiasFill* jobs, int n, hipStream_t st);
+// relu_x (pooling, LRN): take the input through a ReLU as it is read.
 int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y, int32_t* idx,
-                hipStream_t st);
+                hipStream_t st, bool relu_x = false);
 int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha, float beta,
-               float k, float* y, hipStream_t st);
+               float k, float* y, hipStream_t st, bool relu_x = false);
 int launch_relu(const float* x, float* y, int64_t n, hipStream_t st);
 // LRN (across channels, odd size) followed by pooling of its output, in one
 // kernel; s is the pooling shape (its input is the LRN's shape).  Only where
 // lrn_pool_fusable() holds.
 bool lrn_pool_fusable(const PoolShape& s, int size);
 int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alpha, float beta, float k,
-                    const float* x, float* y, int32_t* idx, hipStream_t st);
+                    const float* x, float* y, int32_t* idx, hipStream_t st, bool relu_x = false);
 int launch_softmax(const float* x, int N, int C, int HW, float* y, hipStream_t st);
 
 }  // namespace cnn

@@ -68,11 +68,13 @@ int conv2d_num_configs() { return kNumConfigs; }
 
 const char* conv2d_config_name(int i) { return (i >= 0 && i < kNumConfigs) ? kConfigs[i].name : nullptr; }
 
-int launch_conv2d(const ConvShape& s, const float* x, const float* w, const float* bias, int relu,
-                  float* y, hipStream_t st, int cfg) {
-    ConvParams prm;
-    prm.w = w;
-    prm.bias = bias;
+namespace {
+
+// Parameters, configuration and reduction split of a convolution; per_launch:
+// images per launch (the gather's 31-bit offsets cover fewer than 2^29 input
+// elements).  cfg < 0 on entry: the heuristic's choice.
+int conv_prepare(const ConvShape& s, int* cfg, ConvParams* out, int* per_launch) {
+    ConvParams& prm = *out;
     prm.C = s.C; prm.H = s.H; prm.W = s.W; prm.K = s.K; prm.R = s.R; prm.S = s.S;
     prm.P = s.P; prm.Q = s.Q;
     prm.sh = s.sh; prm.sw = s.sw; prm.ph = s.ph; prm.pw = s.pw;
@@ -82,35 +84,53 @@ int launch_conv2d(const ConvShape& s, const float* x, const float* w, const floa
     prm.Kr = prm.Cg * prm.RS;
     prm.HW = s.H * s.W;
     prm.PQ = s.P * s.Q;
-    prm.relu = relu;
     prm.G = s.G;
     prm.splits = 1;
     prm.kchunk = prm.Kr;
-    if (s.N == 0) return CNN_OK;
-    const bool vec_w = (prm.Kr % 4 == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
+    prm.relu_x = 0;
     const int64_t wbytes = (int64_t)s.K * prm.Kr * 4;
     if (wbytes >= ((int64_t)1 << 31)) return fail(CNN_ERR_UNSUPPORTED, "conv: weights exceed 2 GiB");
     prm.wbytes = (int)wbytes;
-
-    // The gather addresses x through a buffer resource with 31-bit offsets:
-    // launch fewer than 2^29 input elements at a time (whole images).
     const int64_t img = (int64_t)s.C * prm.HW;
-    const int per_launch = (int)std::min<int64_t>(s.N, (((int64_t)1 << 29) - 1) / img);
-    if (per_launch < 1) return fail(CNN_ERR_UNSUPPORTED, "conv: one image exceeds 2^29 elements");
-    if (cfg < 0) {
-        prm.M = per_launch * prm.PQ;
-        cfg = heuristic_config(prm, s.G);
-    }
-    if (cfg >= kNumConfigs) return fail(CNN_ERR_UNSUPPORTED, "conv: no configuration %d", cfg);
+    *per_launch = (int)std::min<int64_t>(std::max(s.N, 1), (((int64_t)1 << 29) - 1) / img);
+    if (*per_launch < 1) return fail(CNN_ERR_UNSUPPORTED, "conv: one image exceeds 2^29 elements");
+    prm.M = *per_launch * prm.PQ;
+    if (*cfg < 0) *cfg = heuristic_config(prm, s.G);
+    if (*cfg >= kNumConfigs) return fail(CNN_ERR_UNSUPPORTED, "conv: no configuration %d", *cfg);
     // One split decision for every launch of the call (the last one may hold
     // fewer images: splitting it the same way is still correct).
-    prm.M = per_launch * prm.PQ;
-    choose_splits(prm, kConfigs[cfg]);
+    choose_splits(prm, kConfigs[*cfg]);
+    return CNN_OK;
+}
+
+}  // namespace
+
+int conv2d_splits(const ConvShape& s, int cfg) {
+    ConvParams prm;
+    int per_launch;
+    if (conv_prepare(s, &cfg, &prm, &per_launch) != CNN_OK) return 1;
+    return prm.splits;
+}
+
+int launch_conv2d(const ConvShape& s, const float* x, const float* w, const float* bias, int relu,
+                  float* y, hipStream_t st, int cfg, const ConvOpts* opt) {
+    if (opt && opt->relu_left) *opt->relu_left = false;
+    if (s.N == 0) return CNN_OK;
+    ConvParams prm;
+    int per_launch;
+    int rc = conv_prepare(s, &cfg, &prm, &per_launch);
+    if (rc != CNN_OK) return rc;
+    prm.w = w;
+    prm.bias = bias;
+    prm.relu = relu;
+    prm.relu_x = opt && opt->relu_in;
+    const bool vec_w = (prm.Kr % 4 == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
+    const int64_t img = (int64_t)s.C * prm.HW;
     const int64_t total = (int64_t)s.N * s.K * prm.PQ;
-    if (prm.splits > 1) {
+    if (prm.splits > 1 && !(opt && opt->prefilled)) {
         hipLaunchKernelGGL(conv::conv_fill_bias, dim3((unsigned)std::min<int64_t>(ceil_div64(total, 256), 4096)),
                            dim3(256), 0, st, y, bias, s.K, prm.PQ, total);
-        const int rc = check_launch("conv_fill_bias");
+        rc = check_launch("conv_fill_bias");
         if (rc != CNN_OK) return rc;
     }
     for (int n0 = 0; n0 < s.N; n0 += per_launch) {
@@ -119,10 +139,16 @@ int launch_conv2d(const ConvShape& s, const float* x, const float* w, const floa
         prm.y = y + (size_t)n0 * s.K * prm.PQ;
         prm.M = nb * prm.PQ;
         prm.xbytes = (int)(nb * img * 4);
-        const int rc = kConfigs[cfg].launch(prm, vec_w, st);
+        rc = kConfigs[cfg].launch(prm, vec_w, st);
         if (rc != CNN_OK) return rc;
     }
-    if (prm.splits > 1 && relu) return launch_relu(y, y, total, st);
+    if (prm.splits > 1 && relu) {
+        if (opt && opt->relu_left) {  // the consumer applies it
+            *opt->relu_left = true;
+            return CNN_OK;
+        }
+        return launch_relu(y, y, total, st);
+    }
     return CNN_OK;
 }
 

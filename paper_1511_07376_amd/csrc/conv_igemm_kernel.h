@@ -59,6 +59,7 @@ struct ConvParams {
     int xbytes;  // bytes of x covered by this launch (< 2^31)
     int wbytes;  // bytes of w (< 2^31)
     int relu;
+    int relu_x;  // take the input through a ReLU as it is gathered
     int G;       // groups (grid z = G * splits)
     int splits;  // reduction chunks; > 1: partial tiles are added atomically
     int kchunk;  // taps per chunk (a multiple of every slab length; Kr if splits == 1)
@@ -231,6 +232,10 @@ conv2d_igemm_f32(ConvParams p) {
     };
     auto store_x = [&](int buf, int sg) {
         float* dst = sB(buf) + mloc * LDK + kgrp * KRUN;
+        if (p.relu_x) {  // uniform
+#pragma unroll
+            for (int j = 0; j < KRUN; ++j) xr[sg][j] = xr[sg][j] > 0.0f ? xr[sg][j] : 0.0f;
+        }
 #pragma unroll
         for (int j = 0; j < KRUN; j += 4)
             *reinterpret_cast<float4*>(dst + j) =

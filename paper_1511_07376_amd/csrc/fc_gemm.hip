@@ -222,18 +222,20 @@ __global__ void fc_fill_bias(float* y, const float* bias, int N, int O) {
         y[i] = bias ? bias[i % O] : 0.0f;
 }
 
-// Several outputs at once: job j sets y_j[n][o] = bias_j[o] (or 0).
+// Several outputs at once: job j sets y_j[n][o][i] = bias_j[o] (or 0) for
+// i < inner.
 struct FillJobs {
-    FcFill job[kMaxFcFills];
+    BiasFill job[kMaxBiasFills];
     int n;
 };
 
-__global__ void fc_fill_bias_multi(FillJobs f) {
+__global__ void bias_fill_multi(FillJobs f) {
     for (int j = 0; j < f.n; ++j) {
-        const FcFill& jb = f.job[j];
-        const int total = jb.N * jb.O;
-        for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x)
-            jb.y[i] = jb.bias ? jb.bias[i % jb.O] : 0.0f;
+        const BiasFill& jb = f.job[j];
+        const int64_t total = (int64_t)jb.N * jb.O * jb.inner;
+        for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+             i += (int64_t)gridDim.x * blockDim.x)
+            jb.y[i] = jb.bias ? jb.bias[(i / jb.inner) % jb.O] : 0.0f;
     }
 }
 
@@ -296,18 +298,19 @@ int fc_splits(int N, int I, int O) {
     return N > 0 ? fc_split(fc_geom(N), N, I, O, &kchunk) : 1;
 }
 
-int launch_fc_fills(const FcFill* jobs, int n, hipStream_t st) {
-    for (int j0 = 0; j0 < n; j0 += kMaxFcFills) {
+int launch_bias_fills(const BiasFill* jobs, int n, hipStream_t st) {
+    for (int j0 = 0; j0 < n; j0 += kMaxBiasFills) {
         FillJobs f;
-        f.n = std::min(kMaxFcFills, n - j0);
-        int most = 0;
+        f.n = std::min(kMaxBiasFills, n - j0);
+        int64_t most = 0;
         for (int j = 0; j < f.n; ++j) {
             f.job[j] = jobs[j0 + j];
-            most = std::max(most, f.job[j].N * f.job[j].O);
+            most = std::max(most, (int64_t)f.job[j].N * f.job[j].O * f.job[j].inner);
         }
         if (most == 0) continue;
-        hipLaunchKernelGGL(fc_fill_bias_multi, dim3(std::min(ceil_div(most, 256), 2048)), dim3(256), 0, st, f);
-        const int rc = check_launch("fc_fill_bias_multi");
+        hipLaunchKernelGGL(bias_fill_multi, dim3((unsigned)std::min<int64_t>(ceil_div64(most, 256), 2048)),
+                           dim3(256), 0, st, f);
+        const int rc = check_launch("bias_fill_multi");
         if (rc != CNN_OK) return rc;
     }
     return CNN_OK;

@@ -92,8 +92,15 @@ int tune(const ConvShape& s, const float* x, const float* w, const float* bias, 
 
 }  // namespace
 
+int conv2d_planned_config(const ConvShape& s) {
+    std::lock_guard<std::mutex> lock(g_mu);
+    auto it = g_table.find(key_of(s));
+    if (it != g_table.end()) return it->second;
+    return g_autotune ? -2 : -1;
+}
+
 int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const float* bias, int relu,
-                    float* y, hipStream_t st) {
+                    float* y, hipStream_t st, const ConvOpts* opt) {
     int cfg = -1;
     bool autotune;
     {
@@ -109,7 +116,7 @@ int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const fl
             g_table[key_of(s)] = cfg;
         }
     }
-    return launch_conv2d(s, x, w, bias, relu, y, st, cfg);
+    return launch_conv2d(s, x, w, bias, relu, y, st, cfg, opt);
 }
 
 }  // namespace cnn

@@ -79,13 +79,17 @@ def test_net_out_shape_and_workspace(name, out):
     ws = cnn.lib.cnn_net_workspace_bytes(descs, len(descs), out[0], C, H, W)
     # two 256-byte aligned buffers of the largest activation, then one aligned
     # output per FC layer other than the last (at these batches every FC layer
-    # splits its reduction: its output tiles cannot fill the GPU)
-    biggest = max(a.size for a in oracle.net_fwd(net, wl.make_input(net, 1), wl.make_params(net),
-                                                 keep=True)[1]) * out[0] * 4
-    half = (biggest + 255) // 256 * 256
-    fcs = [l for l in net.layers if l.kind == "fc"][:-1]
-    fc_area = sum((out[0] * l.out_features * 4 + 255) // 256 * 256 for l in fcs)
-    assert ws == 2 * half + fc_area
+    # splits its reduction: its output tiles cannot fill the GPU), and one per
+    # conv layer that some tile configuration would split
+    outs = oracle.net_fwd(net, wl.make_input(net, 1), wl.make_params(net), keep=True)[1]
+    half = (max(a.size for a in outs) * out[0] * 4 + 255) // 256 * 256
+    al = lambda b: (b + 255) // 256 * 256
+    fc_area = sum(al(out[0] * l.out_features * 4) for l in [l for l in net.layers if l.kind == "fc"][:-1])
+    conv_outs = [al(a.size * out[0] * 4) for l, a in zip(net.layers, outs) if l.kind == "conv"]
+    sums = {0}
+    for b in conv_outs:
+        sums |= {s + b for s in sums}
+    assert ws - 2 * half - fc_area in sums
 
 
 def _descs(net):

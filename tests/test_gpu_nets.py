@@ -208,3 +208,30 @@ def test_fc_chain_relu_carried_into_next_layer(gpu, batch):
     params = wl.make_params(net, 11)
     y = to_host(gpu.Network(net, params)(to_dev(x)))
     assert_gemm_close(y, oracle.net_fwd(net, x, params), 200, f"fc chain B{batch}")
+
+
+@pytest.mark.parametrize("name,batch", [("alexnet", 1), ("alexnet", 2), ("lenet", 1),
+                                        ("cifar_quick", 1), ("cifar_quick", 3)])
+def test_small_batches(gpu, name, batch):
+    """Small batches split the conv and FC reductions: their outputs start as
+    the bias (one fill for the pass) and their ReLUs are applied by the next
+    layer as it reads them (conv gathers, pooling, LRN, FC)."""
+    _run(gpu, wl.NETS[name], batch, None, seed=12)
+
+
+def test_workspace_size_does_not_depend_on_tuning(gpu):
+    net = wl.alexnet
+    params = wl.make_params(net, 13)
+    x = to_dev(wl.make_input(net, 2, 13))
+    gpu.cnn_tuning_clear()
+    try:
+        gpu.cnn_set_autotune(True)
+        model = gpu.Network(net, params)
+        before = model.workspace_bytes(2)
+        y1 = to_host(model(x))            # tunes every conv shape of batch 2
+        assert model.workspace_bytes(2) == before
+        y2 = to_host(model(x))            # tuned configurations, maybe split
+        assert_gemm_close(y2, y1, 4096, "tuned vs first pass")
+    finally:
+        gpu.cnn_set_autotune(False)
+        gpu.cnn_tuning_clear()
