@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <vector>
 
 namespace cnn {
 namespace {
@@ -243,15 +244,13 @@ __global__ void __launch_bounds__(kThreads) lrn_across_f32(LrnParams p) {
 // LRN followed by pooling in one pass, for the network executor (an LRN layer
 // whose output only feeds a pooling layer): the LRN output never goes to
 // memory.  A workgroup takes one image, CB channels and a band of PB pooling
-// output rows:
-//   1. loads the band's input rows of its channels plus the LRN halo into LDS
-//      (every load of a thread in flight at once; channels and rows outside
-//      the tensor read 0),
-//   2. computes each LRN value once, in place: a thread walks the channels
-//      of one (row, column) of the band with the window in registers and
-//      writes channel c's value over its input once no later window needs
-//      it (same arithmetic as the LRN kernel),
-//   3. pools from the tile (same order and comparisons as the pooling
+// output rows (RB input rows):
+//   1. each work-item is one pixel of the band and CC consecutive channels:
+//      it loads those channels plus the HALF-channel halo on each side
+//      straight into registers (every load in flight at once; channels and
+//      rows outside the tensor read 0) and writes the CC LRN values to LDS,
+//      with the same arithmetic as the LRN kernel;
+//   2. pools from the LDS tile (same order and comparisons as the pooling
 //      kernels), so the result equals the two layers run one after the other,
 //      bit for bit.
 struct LrnPoolParams {
@@ -267,11 +266,11 @@ struct LrnPoolParams {
     float alpha_over_size, beta, k;
 };
 
-template <int HALF, int MODE, bool WITH_IDX>  // MODE 0: max, 1: average
+template <int HALF, int CC, int MODE, bool WITH_IDX>  // MODE 0: max, 1: average
 __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
     constexpr int WIN = 2 * HALF + 1;
-    extern __shared__ float in[];           // [CB + 2 HALF][RB][W]
-    const int CIN = p.CB + 2 * HALF;        // channels staged
+    constexpr int NV = CC + 2 * HALF;       // channels loaded per work-item
+    extern __shared__ float lrn[];          // [CB][RB][W]
     int b = blockIdx.x;
     const int band = b % p.nband;
     b /= p.nband;
@@ -284,48 +283,32 @@ __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
     const int HW = p.H * p.W;
     const int plane = p.RB * p.W;
 
-    // 1. stage the input: element e = (j, r, w), channel c0 - HALF + j, row row0 + r
+    // 1. LRN of the band: work-item (s, r, w) is channels c0 + s CC .. + CC - 1
+    //    at input row row0 + r, column w
     const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(p.x + (size_t)n * p.C * HW), (short)0, 0x7fffffff, 0x00020000);
-    const int nin = CIN * plane;
-    constexpr int kBurst = 32;
-    for (int e0 = threadIdx.x; e0 < nin; e0 += kBurst * kThreads) {
-        float v[kBurst];
+    const int nitem = (p.CB / CC) * plane;
+    for (int it = threadIdx.x; it < nitem; it += kThreads) {
+        const int s = (int)fdiv(it, p.f_plane);
+        const int rw = it - s * plane;
+        const int r = (int)fdiv(rw, p.f_w);
+        const int h = row0 + r;
+        const int pix = h * p.W + (rw - r * p.W);
+        const int cs = c0 + s * CC - HALF;  // channel of v[0]
+        const bool hok = (unsigned)h < (unsigned)p.H;
+        float v[NV];
 #pragma unroll
-        for (int u = 0; u < kBurst; ++u) {
-            const int e = e0 + u * kThreads;
-            const int j = (int)fdiv(e, p.f_plane);
-            const int rw = e - j * plane;
-            const int r = (int)fdiv(rw, p.f_w);
-            const int w = rw - r * p.W;
-            const int c = c0 - HALF + j;
-            const int h = row0 + r;
-            const bool ok = e < nin && (unsigned)c < (unsigned)p.C && (unsigned)h < (unsigned)p.H;
-            const int off = ok ? (c * HW + h * p.W + w) * 4 : (int)0x80000000u;
-            v[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0));
+        for (int j = 0; j < NV; ++j) {
+            const int c = cs + j;
+            const int off = hok && (unsigned)c < (unsigned)p.C ? (c * HW + pix) * 4 : (int)0x80000000u;
+            v[j] = relu_in(__builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0)),
+                           p.relu_x);
         }
+        float* out = lrn + s * CC * plane + rw;
 #pragma unroll
-        for (int u = 0; u < kBurst; ++u)
-            if (e0 + u * kThreads < nin) in[e0 + u * kThreads] = relu_in(v[u], p.relu_x);
+        for (int i = 0; i < CC; ++i) out[i * plane] = lrn_value<WIN>(&v[i], p.k, p.alpha_over_size, p.beta);
     }
     __syncthreads();
-
-    // 2. LRN of the CB channels over the band, in place: channel c's value
-    //    goes to staged channel c + HALF, read into the window at step c - HALF
-    for (int rw = threadIdx.x; rw < plane; rw += kThreads) {
-        float win[WIN];
-#pragma unroll
-        for (int j = 0; j < WIN - 1; ++j) win[j] = in[j * plane + rw];
-        for (int c = 0; c < p.CB; ++c) {
-            win[WIN - 1] = in[(c + WIN - 1) * plane + rw];
-            const float v = lrn_value<WIN>(win, p.k, p.alpha_over_size, p.beta);
-            in[(c + HALF) * plane + rw] = v;
-#pragma unroll
-            for (int j = 0; j < WIN - 1; ++j) win[j] = win[j + 1];
-        }
-    }
-    __syncthreads();
-    const float* lrn = in + HALF * plane;  // [CB][RB][W]
 
     // 3. pooling from the LRN tile
     const int PQ = p.P * p.Q;
@@ -504,56 +487,76 @@ int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha
 }
 
 namespace {
-constexpr int kLrnPoolLds = 32 * 1024;  // LDS budget of one fused workgroup (4+ per CU)
+struct LrnPoolTiling {
+    int CB, CC, PB, RB;
+    int64_t blocks;
+};
 
-// Channels and output rows per workgroup of the fused LRN + pooling kernel:
-// among the tilings that fit the LDS budget, the one that reads the fewest
-// input elements per output (channel halo and overlapping band rows are read
-// twice); false when none fits.
-bool lrn_pool_tiling(const PoolShape& s, int half, int* CB, int* PB, int* RB) {
-    double best = 1e30;
-    for (int cb : {32, 16, 8, 4}) {
-        if (cb > 4 && cb / 2 >= s.C) continue;  // no wider than the channels need
-        for (int pb = std::min(s.P, 16); pb >= 1; --pb) {
-            const int rb = (pb - 1) * s.sh + s.kh;
-            const int64_t bytes = (int64_t)(cb + 2 * half) * rb * s.W * 4;
-            if (bytes > kLrnPoolLds) continue;
-            const double cost = (double)(cb + 2 * half) * rb / ((double)std::min(cb, s.C) * pb);
-            if (cost < best - 1e-9) {
-                best = cost;
-                *CB = cb;
-                *PB = pb;
-                *RB = rb;
+// Channels (CB, with CC = CB per work-item) and output rows per workgroup of
+// the fused LRN + pooling kernel.  The kernel is bound by how many loads are
+// in flight, so occupancy comes first: a workgroup keeps its LDS tile within
+// 20 KB, which lets 8 workgroups (32 waves) share a CU; only shapes with no
+// such tiling go up to 40 KB.  Among those tilings the cheapest reads the
+// fewest input elements per LRN value it keeps (channel halo times
+// overlapping band rows), with ragged passes of the workgroup over its
+// work-items counted in full.  A launch needs enough workgroups to fill the
+// chip: tilings giving fewer than 1024 (or than the most any tiling gives,
+// for small batches) are passed over.  False when nothing fits.
+bool lrn_pool_tiling(const PoolShape& s, int half, LrnPoolTiling* t) {
+    for (int budget : {20 * 1024, 40 * 1024}) {
+        std::vector<LrnPoolTiling> cand;
+        std::vector<double> cost;
+        int64_t most = 0;
+        for (int cb : {16, 8}) {
+            if (cb > 8 && cb / 2 >= s.C) continue;  // no wider than the channels need
+            for (int pb = 1; pb <= std::min(s.P, 16); ++pb) {
+                const int rb = (pb - 1) * s.sh + s.kh;
+                if ((int64_t)cb * rb * s.W * 4 > budget) break;
+                const int64_t items = (int64_t)rb * s.W;
+                const double fill = (double)ceil_div64(items, kThreads) * kThreads / (double)items;
+                const double amp = (double)(cb + 2 * half) / std::min(cb, s.C) * rb / ((double)pb * s.sh);
+                cand.push_back({cb, cb, pb, rb, (int64_t)s.N * ceil_div(s.C, cb) * ceil_div(s.P, pb)});
+                cost.push_back(amp * fill);
+                most = std::max(most, cand.back().blocks);
             }
-            break;  // the tallest band that fits is the cheapest for this cb
         }
+        const int64_t want = std::min<int64_t>(1024, most);
+        double best = 1e30;
+        for (size_t i = 0; i < cand.size(); ++i)
+            if (cand[i].blocks >= want && cost[i] < best - 1e-12) {
+                best = cost[i];
+                *t = cand[i];
+            }
+        if (best < 1e29) return true;
     }
-    return best < 1e29;
+    return false;
 }
 }  // namespace
 
 bool lrn_pool_fusable(const PoolShape& s, int size) {
-    int cb, pb, rb;
+    LrnPoolTiling t;
     if (size % 2 != 1 || size / 2 > 4 || (int64_t)s.C * s.H * s.W >= ((int64_t)1 << 29) ||
-        !lrn_pool_tiling(s, size / 2, &cb, &pb, &rb))
+        !lrn_pool_tiling(s, size / 2, &t))
         return false;
-    // the launch's work-items fit 32 bits
-    const int64_t blocks = (int64_t)s.N * ceil_div(s.C, cb) * ceil_div(s.P, pb);
-    return blocks * kThreads < ((int64_t)1 << 32);
+    return t.blocks * kThreads < ((int64_t)1 << 32);  // the launch's work-items fit 32 bits
 }
 
 int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alpha, float beta, float k,
                     const float* x, float* y, int32_t* idx, hipStream_t st, bool relu_x) {
     if (s.N == 0) return CNN_OK;
     const int half = size / 2;
-    LrnPoolParams p;
-    if (!lrn_pool_fusable(s, size) || !lrn_pool_tiling(s, half, &p.CB, &p.PB, &p.RB))
+    LrnPoolTiling t;
+    if (!lrn_pool_fusable(s, size) || !lrn_pool_tiling(s, half, &t))
         return fail(CNN_ERR_UNSUPPORTED, "lrn+pool: no fused tiling for this shape");
+    LrnPoolParams p;
     p.x = x;
     p.y = y;
     p.idx = idx;
     p.C = s.C; p.H = s.H; p.W = s.W; p.P = s.P; p.Q = s.Q;
     p.kh = s.kh; p.kw = s.kw; p.sh = s.sh; p.sw = s.sw; p.ph = s.ph; p.pw = s.pw;
+    p.CB = t.CB;
+    p.PB = t.PB;
+    p.RB = t.RB;
     p.nchunk = ceil_div(s.C, p.CB);
     p.nband = ceil_div(s.P, p.PB);
     p.f_plane = make_fastdiv(p.RB * s.W);
@@ -565,17 +568,23 @@ int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alph
     p.beta = beta;
     p.k = k;
     p.relu_x = relu_x;
-    const int64_t blocks = (int64_t)s.N * p.nchunk * p.nband;
-    const size_t shm = (size_t)(p.CB + 2 * half) * p.RB * s.W * 4;
-    const dim3 grid((unsigned)blocks), block(kThreads);
-#define CNN_LRN_POOL(H)                                                                          \
+    const size_t shm = (size_t)p.CB * p.RB * s.W * 4;
+    const dim3 grid((unsigned)t.blocks), block(kThreads);
+#define CNN_LRN_POOL_CC(H, CC)                                                                   \
     do {                                                                                         \
         if (mode == CNN_POOL_MAX && idx)                                                         \
-            hipLaunchKernelGGL((lrn_pool_f32<H, 0, true>), grid, block, shm, st, p);             \
+            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 0, true>), grid, block, shm, st, p);         \
         else if (mode == CNN_POOL_MAX)                                                           \
-            hipLaunchKernelGGL((lrn_pool_f32<H, 0, false>), grid, block, shm, st, p);            \
+            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 0, false>), grid, block, shm, st, p);        \
         else                                                                                     \
-            hipLaunchKernelGGL((lrn_pool_f32<H, 1, false>), grid, block, shm, st, p);            \
+            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 1, false>), grid, block, shm, st, p);        \
+    } while (0)
+#define CNN_LRN_POOL(H)                  \
+    do {                                 \
+        if (t.CC == 16)                  \
+            CNN_LRN_POOL_CC(H, 16);      \
+        else                             \
+            CNN_LRN_POOL_CC(H, 8);       \
     } while (0)
     switch (half) {
         case 0: CNN_LRN_POOL(0); break;
@@ -585,6 +594,7 @@ int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alph
         default: CNN_LRN_POOL(4); break;
     }
 #undef CNN_LRN_POOL
+#undef CNN_LRN_POOL_CC
     return check_launch("lrn_pool_f32");
 }
 

@@ -121,21 +121,25 @@ def test_net_output_canary_and_workspace_reuse(gpu):
                           oracle.net_fwd(net, x, wl.make_params(net, 5)), 500, f"lenet B{batch}")
 
 
-@pytest.mark.parametrize("C,H,mode,k,s,p,relu", [
-    (96, 55, "max", 3, 2, 0, False),    # AlexNet layers 2-3 shape
-    (40, 27, "max", 3, 2, 1, True),     # channel count not a multiple of 32, padding, ReLU
-    (7, 13, "avg", 3, 2, 0, False),
-    (33, 9, "max", 2, 2, 0, False),
-    (5, 120, "max", 3, 2, 0, False),
+@pytest.mark.parametrize("C,H,mode,k,s,p,relu,batch", [
+    (96, 55, "max", 3, 2, 0, False, 3),    # AlexNet layers 2-3 shape
+    (40, 27, "max", 3, 2, 1, True, 3),     # channel count not a multiple of 8, padding, ReLU
+    (7, 13, "avg", 3, 2, 0, False, 3),
+    (33, 9, "max", 2, 2, 0, False, 3),
+    (5, 120, "max", 3, 2, 0, False, 3),
+    # batches large enough for 16-channel workgroups
+    (256, 27, "max", 3, 2, 0, False, 16),  # AlexNet layers 6-7 shape
+    (72, 27, "max", 3, 2, 1, True, 64),    # 72 channels: last chunk of 16 ragged
+    (72, 27, "avg", 3, 2, 1, False, 64),
 ])
-def test_lrn_then_pool_matches_separate_layers(gpu, C, H, mode, k, s, p, relu):
+def test_lrn_then_pool_matches_separate_layers(gpu, C, H, mode, k, s, p, relu, batch):
     """An LRN followed by pooling in a network gives values and indices equal,
     bit for bit, to those of the two single-layer calls."""
-    print(f"lrn+pool C{C} H{H} {mode} k{k} s{s} p{p} relu{int(relu)}", flush=True)
+    print(f"lrn+pool C{C} H{H} {mode} k{k} s{s} p{p} relu{int(relu)} batch {batch}", flush=True)
     net = wl.Net("lrn_pool", (C, H, H), (wl.lrn(5, 1e-2, 0.75, 2.0),
                                         wl.pool(mode, k, s, p, relu=relu)),
                  weight_std=0.0, bias_std=0.0, input_dist="normal")
-    x = wl.make_input(net, 3, 8) * 4
+    x = wl.make_input(net, batch, 8) * 4
     model = gpu.Network(net, wl.make_params(net, 8), pool_index=(mode == "max"))
     xd = to_dev(x)
     y = to_host(model(xd))
