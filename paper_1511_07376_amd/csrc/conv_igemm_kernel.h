@@ -95,7 +95,7 @@ conv2d_igemm_f32(ConvParams p) {
     constexpr int LDK = BK + 4;        // padded LDS row (conflict-free 128-bit reads)
     constexpr int KGROUPS = NT / TN;   // threads sharing one pixel column of the gather
     constexpr int KRUN = BK / KGROUPS; // consecutive taps gathered per thread
-    static_assert(NT % TN == 0 && TN >= 64, "gather layout needs TN | NT and TN >= 64");
+    static_assert(NT % TN == 0 && TN % 64 == 0, "gather layout needs TN | NT and whole waves per pixel column");
     static_assert(BK % KGROUPS == 0 && KRUN % 4 == 0, "gather run must be whole float4s");
     static_assert(BK % 8 == 0, "slab must split into two halves of float4s");
     constexpr int WTOT = VEC_W ? TM * BK / 4 : TM * BK;  // weight-tile loads per slab
@@ -134,7 +134,7 @@ conv2d_igemm_f32(ConvParams p) {
 
     // ---- gather setup: this thread's pixel and tap run (fixed for all slabs)
     const int mloc = tid % TN;
-    const int kgrp = __builtin_amdgcn_readfirstlane(tid / TN);  // uniform: TN >= 64
+    const int kgrp = __builtin_amdgcn_readfirstlane(tid / TN);  // uniform: TN is a multiple of 64
     const int m = m0 + mloc;
     int hb, wb, lane_off;
     if (m < p.M) {
