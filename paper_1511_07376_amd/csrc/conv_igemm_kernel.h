@@ -77,7 +77,13 @@ struct ConvParams {
 //  kGatherNoPad: no padding, so every tap of an in-range pixel lies inside
 //    the image.  The table holds byte offsets (2^31 past the reduction) and
 //    out-of-range pixels start at 2^31: an element costs one add.
-constexpr int kGatherScalar = 0, kGatherMask = 1, kGatherNoPad = 2;
+//  kGatherStrided: no padding and a column stride above 1.  Same table, but
+//    one load instruction covers 16 neighbouring pixels x 4 consecutive taps
+//    (lane l: pixel l/4, tap l%4) instead of 64 pixels x 1 tap: with
+//    neighbouring pixels `stride` floats apart, the 64 addresses then span 2-3
+//    cache lines rather than 8, which is what limits a stride-4 stem.  A
+//    thread holds KRUN*4/BK pixels and reads its taps' table entries per lane.
+constexpr int kGatherScalar = 0, kGatherMask = 1, kGatherNoPad = 2, kGatherStrided = 3;
 
 // KS > 1: the workgroup holds KS groups of WMW x WNW waves that reduce
 // interleaved slabs (group g takes slabs g, g + KS, ...) into the same
@@ -86,6 +92,7 @@ constexpr int kGatherScalar = 0, kGatherMask = 1, kGatherNoPad = 2;
 // shrinking each wave's tile.
 template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W, int GATHER, int KS, int ST>
 __global__ void __launch_bounds__(64 * WMW * WNW * KS)
+__attribute__((amdgpu_waves_per_eu(GATHER == kGatherStrided && FM * FN <= 3 ? 4 : 1)))
 conv2d_igemm_f32(ConvParams p) {
     static_assert(ST % 2 == 0, "the two LDS buffers alternate within a round of ST slabs");
     constexpr int TM = WMW * FM * 32;  // output channels per workgroup
@@ -181,10 +188,48 @@ conv2d_igemm_f32(ConvParams p) {
                         inv |= 1u << (r * p.S + s);
         }
     }
+    // strided gather: element u of a thread is pixel group u / TG (16 pixels
+    // apart) and tap group u % TG (4 taps apart) of its wave's pixels
+    constexpr int TG = BK / 4;          // tap groups per slab
+    constexpr int PPT = KRUN / TG;      // pixels per thread
+    constexpr int PW = 16 * PPT;        // pixels per wave
+    static_assert(GATHER != kGatherStrided || (KRUN % TG == 0 && (NT / 64) * PW == TN),
+                  "strided gather: whole pixel groups per wave");
+    const int ln = tid & 63;
+    const int wpix = (tid >> 6) * PW + (ln >> 2);  // this thread's first pixel, within the tile
+    int soff[GATHER == kGatherStrided ? PPT : 1];
+    if constexpr (GATHER == kGatherStrided) {
+#pragma unroll
+        for (int pi = 0; pi < PPT; ++pi) {
+            const int mm = m0 + wpix + pi * 16;
+            if (mm < p.M) {
+                const int n = mm / p.PQ;
+                const int pq = mm - n * p.PQ;
+                const int pp = pq / p.Q;
+                const int qq = pq - pp * p.Q;
+                soff[pi] = ((n * p.C + g * p.Cg) * p.HW + pp * p.sh * p.W + qq * p.sw) * 4;
+            } else {
+                soff[pi] = (int)0x80000000u;
+            }
+        }
+    }
     if constexpr (GATHER != kGatherScalar) __syncthreads();
 
     float xr[ST][KRUN];  // register stages
     auto load_x = [&](int kslab, int sg) {
+        if constexpr (GATHER == kGatherStrided) {
+#pragma unroll
+            for (int q = 0; q < TG; ++q) {
+                const int e = stab[kslab + 4 * q + (ln & 3)];
+#pragma unroll
+                for (int pi = 0; pi < PPT; ++pi) {
+                    const int voff = (int)((unsigned)soff[pi] + (unsigned)e);
+                    xr[sg][pi * TG + q] =
+                        __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, voff, 0, 0));
+                }
+            }
+            return;
+        }
         const int kk0 = kslab + kgrp * KRUN;  // uniform
         if constexpr (GATHER != kGatherScalar) {
 #pragma unroll
@@ -231,11 +276,17 @@ conv2d_igemm_f32(ConvParams p) {
         }
     };
     auto store_x = [&](int buf, int sg) {
-        float* dst = sB(buf) + mloc * LDK + kgrp * KRUN;
         if (p.relu_x) {  // uniform
 #pragma unroll
             for (int j = 0; j < KRUN; ++j) xr[sg][j] = xr[sg][j] > 0.0f ? xr[sg][j] : 0.0f;
         }
+        if constexpr (GATHER == kGatherStrided) {
+            float* dst = sB(buf) + wpix * LDK + (ln & 3);
+#pragma unroll
+            for (int u = 0; u < KRUN; ++u) dst[(u / TG) * 16 * LDK + 4 * (u % TG)] = xr[sg][u];
+            return;
+        }
+        float* dst = sB(buf) + mloc * LDK + kgrp * KRUN;
 #pragma unroll
         for (int j = 0; j < KRUN; j += 4)
             *reinterpret_cast<float4*>(dst + j) =
@@ -449,16 +500,18 @@ int launch_cfg(const ConvParams& prm, bool vec_w, hipStream_t st) {
     const bool tab_fits = tab_entries * 4 <= 32768;
     int mode = kGatherScalar;
     if (tab_fits && prm.ph == 0 && prm.pw == 0)
-        mode = kGatherNoPad;
+        mode = prm.sw > 1 ? kGatherStrided : kGatherNoPad;
     else if (tab_fits && prm.RS <= 31 && (int64_t)prm.Cg * prm.HW * 4 < ((int64_t)1 << 27))
         mode = kGatherMask;
     const size_t shm = mode == kGatherScalar ? 0 : (size_t)tab_entries * 4;
     if (vec_w) {
-        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherNoPad>(prm, grid, block, shm, st);
+        if (mode == kGatherStrided) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherStrided>(prm, grid, block, shm, st);
+        else if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherNoPad>(prm, grid, block, shm, st);
         else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherMask>(prm, grid, block, shm, st);
         else launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherScalar>(prm, grid, block, shm, st);
     } else {
-        if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherNoPad>(prm, grid, block, shm, st);
+        if (mode == kGatherStrided) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherStrided>(prm, grid, block, shm, st);
+        else if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherNoPad>(prm, grid, block, shm, st);
         else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherMask>(prm, grid, block, shm, st);
         else launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherScalar>(prm, grid, block, shm, st);
     }

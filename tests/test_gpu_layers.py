@@ -283,7 +283,8 @@ CFG_SHAPES = [
     # N, C, H, W, K, R, S, stride, pad, G
     # reductions divisible by 4 (128-bit weight loads) and not (32-bit loads);
     # gather modes: padded filters of <= 31 taps (mask), unpadded (no-pad),
-    # padded 7x7 and a reduction too long for the LDS tap table (scalar)
+    # unpadded with a stride (strided), padded 7x7 and a reduction too long
+    # for the LDS tap table (scalar)
     (2, 8, 12, 13, 70, 3, 3, 1, 1, 1),
     (2, 32, 9, 9, 130, 1, 1, 1, 0, 2),
     (2, 3, 23, 21, 40, 7, 7, 2, 3, 1),
@@ -291,6 +292,8 @@ CFG_SHAPES = [
     (2, 5, 13, 11, 70, 3, 3, 1, 1, 1),
     (3, 6, 17, 19, 130, 5, 5, 2, 2, 2),
     (1, 3, 31, 29, 97, 11, 11, 4, 0, 1),
+    (2, 4, 19, 23, 40, 3, 3, 2, 0, 1),     # strided gathers: stride 2, 128-bit weight loads
+    (1, 6, 40, 37, 70, 5, 5, 3, 0, 2),     # stride 3, two groups, ragged pixel tiles
     # few output tiles: the reduction is split across workgroups (mask, no-pad
     # and scalar gathers; chunks that start inside a filter; a ragged last
     # chunk with 32-bit weight loads and two groups)
@@ -298,6 +301,7 @@ CFG_SHAPES = [
     (1, 512, 6, 5, 40, 1, 1, 1, 0, 1),
     (1, 64, 9, 9, 20, 7, 7, 1, 3, 1),
     (1, 100, 5, 5, 30, 3, 3, 1, 1, 2),
+    (1, 96, 15, 15, 40, 3, 3, 2, 0, 1),    # split reduction with the strided gather
 ]
 
 
