@@ -132,6 +132,48 @@ def cpu_baseline(net, x, params, budget_s):
             "value_1_thread": round(1.0 / t_one, 3)}
 
 
+def conv_sweep(args):
+    """Single-layer conv sweep: each case auto-tunes on its first call, then
+    `--steps` launches are timed between two HIP events on the launch stream."""
+    import torch
+    from paper_1511_07376_amd import cnn
+    from paper_1511_07376_amd import workloads as wl
+
+    cnn.cnn_set_autotune(True)
+    for shape in wl.SWEEP_SHAPES:
+        c, h, w_, k, r, s_, stride, pad = shape
+        for n in wl.SWEEP_BATCHES:
+            x, w, b = (torch.from_numpy(t).cuda() for t in wl.make_sweep_tensors(shape, n, args.seed))
+            p, q = cnn.cnn_conv2d_out_shape(h, w_, r, s_, stride, pad)
+            flops = 2.0 * n * k * p * q * c * r * s_
+
+            def timed(fn):
+                for _ in range(max(args.warmup, 1)):
+                    fn()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(args.steps):
+                    fn()
+                e1.record()
+                torch.cuda.synchronize()
+                return e0.elapsed_time(e1) / args.steps
+
+            y = torch.empty(n, k, p, q, device="cuda")
+            ms = timed(lambda: cnn.cnn_conv2d_fwd(x, w, b, stride, pad, 1, True, y=y))
+            tf = flops / (ms * 1e-3) / 1e12
+            rec = {"case": {"C": c, "H": h, "W": w_, "K": k, "R": r, "S": s_, "stride": stride, "pad": pad,
+                            "N": n},
+                   "us": round(ms * 1e3, 2), "gflop": round(flops / 1e9, 4), "tflops": round(tf, 2),
+                   "frac_fp32_mfma": round(tf / PEAK_FP32_MFMA_TFLOPS, 4)}
+            if args.sweep_miopen:
+                import torch.nn.functional as F
+                ms_m = timed(lambda: torch.relu_(F.conv2d(x, w, b, stride, pad)))
+                rec["miopen_us"] = round(ms_m * 1e3, 2)
+            print(json.dumps(rec), flush=True)
+    cnn.cnn_set_autotune(False)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -152,6 +194,11 @@ def main():
                          "(the library's graph execution mode)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the network: time the single-layer conv sweep (five shapes x "
+                         "batches 1, 16, 64, bias + ReLU fused), one JSON line per case")
+    ap.add_argument("--sweep-miopen", action="store_true",
+                    help="with --sweep: also time torch's own conv2d (MIOpen) on the same tensors, as context")
     args = ap.parse_args()
     if args.copy_probe:
         import torch
@@ -161,6 +208,8 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": a.numel() * 4}), flush=True)
         return
+    if args.sweep:
+        return conv_sweep(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the images of a batch are independent: on N GPUs each would run batch/N)",
