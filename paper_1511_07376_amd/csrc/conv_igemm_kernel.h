@@ -83,7 +83,26 @@ struct ConvParams {
 //    neighbouring pixels `stride` floats apart, the 64 addresses then span 2-3
 //    cache lines rather than 8, which is what limits a stride-4 stem.  A
 //    thread holds KRUN*4/BK pixels and reads its taps' table entries per lane.
-constexpr int kGatherScalar = 0, kGatherMask = 1, kGatherNoPad = 2, kGatherStrided = 3;
+//  kGatherStridedMask: the strided layout with padding, for filters of at
+//    most 63 taps: entries are offset << 6 | tap, and each pixel holds a
+//    64-bit mask of its taps outside the image (bit 63: past the reduction).
+constexpr int kGatherScalar = 0, kGatherMask = 1, kGatherNoPad = 2, kGatherStrided = 3, kGatherStridedMask = 4;
+
+// Bit r*S + s set for each tap (r, s) of a filter at input corner (h0, w0)
+// that falls outside the H x W image: one row pattern (the columns outside)
+// per filter row, or the whole row when the row itself is outside.  Needs
+// R*S below the width of T.
+template <typename T>
+__device__ inline T outside_taps(int h0, int w0, int H, int W, int R, int S) {
+    const int lo = max(0, -w0), hi = min(S, W - w0);  // columns s in [lo, hi) are inside
+    const T row = (T(1) << S) - 1;
+    const T inside = hi > lo ? (((T(1) << hi) - 1) & ~((T(1) << lo) - 1)) : T(0);
+    const T cols_out = row & ~inside;
+    T bad = 0;
+    for (int r = 0; r < R; ++r)
+        bad |= ((unsigned)(h0 + r) >= (unsigned)H ? row : cols_out) << (r * S);
+    return bad;
+}
 
 // KS > 1: the workgroup holds KS groups of WMW x WNW waves that reduce
 // interleaved slabs (group g takes slabs g, g + KS, ...) into the same
@@ -166,50 +185,50 @@ conv2d_igemm_f32(ConvParams p) {
     unsigned inv = 0xffffffffu;
     if constexpr (GATHER != kGatherScalar) {
         for (int kk = threadIdx.x; kk < (niter + ST) * KS * BK; kk += NTB) {
-            int e = GATHER == kGatherMask ? 31 : (int)0x80000000u;
+            int e = GATHER == kGatherMask ? 31 : GATHER == kGatherStridedMask ? 63 : (int)0x80000000u;
             if (kk < klen) {
                 const int c = (kbeg + kk) / p.RS;
                 const int rs = kbeg + kk - c * p.RS;
                 const int r = rs / p.S;
                 const int s = rs - r * p.S;
                 const int toff = ((c * p.H + r) * p.W + s) * 4;
-                e = GATHER == kGatherMask ? ((toff << 5) | rs) : toff;
+                e = GATHER == kGatherMask ? ((toff << 5) | rs) : GATHER == kGatherStridedMask ? ((toff << 6) | rs) : toff;
             }
             stab[kk] = e;
         }
         if (GATHER == kGatherNoPad && m >= p.M) lane_off = (int)0x80000000u;
     }
     if constexpr (GATHER == kGatherMask) {
-        if (m < p.M) {
-            inv = 0x80000000u;
-            for (int r = 0; r < p.R; ++r)
-                for (int s = 0; s < p.S; ++s)
-                    if ((unsigned)(hb + r) >= (unsigned)p.H || (unsigned)(wb + s) >= (unsigned)p.W)
-                        inv |= 1u << (r * p.S + s);
-        }
+        if (m < p.M) inv = 0x80000000u | outside_taps<unsigned>(hb, wb, p.H, p.W, p.R, p.S);
     }
     // strided gather: element u of a thread is pixel group u / TG (16 pixels
     // apart) and tap group u % TG (4 taps apart) of its wave's pixels
     constexpr int TG = BK / 4;          // tap groups per slab
     constexpr int PPT = KRUN / TG;      // pixels per thread
     constexpr int PW = 16 * PPT;        // pixels per wave
-    static_assert(GATHER != kGatherStrided || (KRUN % TG == 0 && (NT / 64) * PW == TN),
+    constexpr bool STRIDED = GATHER == kGatherStrided || GATHER == kGatherStridedMask;
+    static_assert(!STRIDED || (KRUN % TG == 0 && (NT / 64) * PW == TN),
                   "strided gather: whole pixel groups per wave");
     const int ln = tid & 63;
     const int wpix = (tid >> 6) * PW + (ln >> 2);  // this thread's first pixel, within the tile
-    int soff[GATHER == kGatherStrided ? PPT : 1];
-    if constexpr (GATHER == kGatherStrided) {
+    int soff[STRIDED ? PPT : 1];
+    unsigned long long inv64[GATHER == kGatherStridedMask ? PPT : 1];
+    if constexpr (STRIDED) {
 #pragma unroll
         for (int pi = 0; pi < PPT; ++pi) {
             const int mm = m0 + wpix + pi * 16;
+            inv64[GATHER == kGatherStridedMask ? pi : 0] = ~0ull;
             if (mm < p.M) {
                 const int n = mm / p.PQ;
                 const int pq = mm - n * p.PQ;
                 const int pp = pq / p.Q;
                 const int qq = pq - pp * p.Q;
-                soff[pi] = ((n * p.C + g * p.Cg) * p.HW + pp * p.sh * p.W + qq * p.sw) * 4;
+                const int h0 = pp * p.sh - p.ph, w0 = qq * p.sw - p.pw;
+                soff[pi] = ((n * p.C + g * p.Cg) * p.HW + h0 * p.W + w0) * 4;
+                if constexpr (GATHER == kGatherStridedMask)
+                    inv64[pi] = (1ull << 63) | outside_taps<unsigned long long>(h0, w0, p.H, p.W, p.R, p.S);
             } else {
-                soff[pi] = (int)0x80000000u;
+                soff[pi] = GATHER == kGatherStridedMask ? 0 : (int)0x80000000u;
             }
         }
     }
@@ -217,13 +236,19 @@ conv2d_igemm_f32(ConvParams p) {
 
     float xr[ST][KRUN];  // register stages
     auto load_x = [&](int kslab, int sg) {
-        if constexpr (GATHER == kGatherStrided) {
+        if constexpr (STRIDED) {
 #pragma unroll
             for (int q = 0; q < TG; ++q) {
                 const int e = stab[kslab + 4 * q + (ln & 3)];
 #pragma unroll
                 for (int pi = 0; pi < PPT; ++pi) {
-                    const int voff = (int)((unsigned)soff[pi] + (unsigned)e);
+                    int voff;
+                    if constexpr (GATHER == kGatherStridedMask) {
+                        const unsigned bad = (unsigned)(inv64[pi] >> (e & 63)) & 1u;
+                        voff = (soff[pi] + (e >> 6)) | (int)(bad << 31);
+                    } else {
+                        voff = (int)((unsigned)soff[pi] + (unsigned)e);
+                    }
                     xr[sg][pi * TG + q] =
                         __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, voff, 0, 0));
                 }
@@ -280,7 +305,7 @@ conv2d_igemm_f32(ConvParams p) {
 #pragma unroll
             for (int j = 0; j < KRUN; ++j) xr[sg][j] = xr[sg][j] > 0.0f ? xr[sg][j] : 0.0f;
         }
-        if constexpr (GATHER == kGatherStrided) {
+        if constexpr (STRIDED) {
             float* dst = sB(buf) + wpix * LDK + (ln & 3);
 #pragma unroll
             for (int u = 0; u < KRUN; ++u) dst[(u / TG) * 16 * LDK + 4 * (u % TG)] = xr[sg][u];
@@ -501,16 +526,20 @@ int launch_cfg(const ConvParams& prm, bool vec_w, hipStream_t st) {
     int mode = kGatherScalar;
     if (tab_fits && prm.ph == 0 && prm.pw == 0)
         mode = prm.sw > 1 ? kGatherStrided : kGatherNoPad;
+    else if (tab_fits && prm.sw > 1 && prm.RS <= 63 && (int64_t)prm.Cg * prm.HW * 4 < ((int64_t)1 << 25))
+        mode = kGatherStridedMask;
     else if (tab_fits && prm.RS <= 31 && (int64_t)prm.Cg * prm.HW * 4 < ((int64_t)1 << 27))
         mode = kGatherMask;
     const size_t shm = mode == kGatherScalar ? 0 : (size_t)tab_entries * 4;
     if (vec_w) {
-        if (mode == kGatherStrided) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherStrided>(prm, grid, block, shm, st);
+        if (mode == kGatherStridedMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherStridedMask>(prm, grid, block, shm, st);
+        else if (mode == kGatherStrided) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherStrided>(prm, grid, block, shm, st);
         else if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherNoPad>(prm, grid, block, shm, st);
         else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherMask>(prm, grid, block, shm, st);
         else launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, true, kGatherScalar>(prm, grid, block, shm, st);
     } else {
-        if (mode == kGatherStrided) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherStrided>(prm, grid, block, shm, st);
+        if (mode == kGatherStridedMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherStridedMask>(prm, grid, block, shm, st);
+        else if (mode == kGatherStrided) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherStrided>(prm, grid, block, shm, st);
         else if (mode == kGatherNoPad) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherNoPad>(prm, grid, block, shm, st);
         else if (mode == kGatherMask) launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherMask>(prm, grid, block, shm, st);
         else launch_kernel<WMW, WNW, FM, FN, BK, KS, ST, false, kGatherScalar>(prm, grid, block, shm, st);

@@ -283,8 +283,9 @@ CFG_SHAPES = [
     # N, C, H, W, K, R, S, stride, pad, G
     # reductions divisible by 4 (128-bit weight loads) and not (32-bit loads);
     # gather modes: padded filters of <= 31 taps (mask), unpadded (no-pad),
-    # unpadded with a stride (strided), padded 7x7 and a reduction too long
-    # for the LDS tap table (scalar)
+    # unpadded with a stride (strided), padded with a stride (strided mask,
+    # 7x7 and 5x5), padded stride-1 7x7 and a reduction too long for the LDS
+    # tap table (scalar)
     (2, 8, 12, 13, 70, 3, 3, 1, 1, 1),
     (2, 32, 9, 9, 130, 1, 1, 1, 0, 2),
     (2, 3, 23, 21, 40, 7, 7, 2, 3, 1),
@@ -302,6 +303,7 @@ CFG_SHAPES = [
     (1, 64, 9, 9, 20, 7, 7, 1, 3, 1),
     (1, 100, 5, 5, 30, 3, 3, 1, 1, 2),
     (1, 96, 15, 15, 40, 3, 3, 2, 0, 1),    # split reduction with the strided gather
+    (1, 64, 17, 17, 40, 3, 3, 2, 1, 1),    # split reduction with the strided, padded gather
 ]
 
 
