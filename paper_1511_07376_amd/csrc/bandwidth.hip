@@ -271,11 +271,19 @@ __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
     constexpr int WIN = 2 * HALF + 1;
     constexpr int NV = CC + 2 * HALF;       // channels loaded per work-item
     extern __shared__ float lrn[];          // [CB][RB][W]
-    int b = blockIdx.x;
-    const int band = b % p.nband;
-    b /= p.nband;
+    // Workgroups go to the 8 XCDs in turn by id, each XCD with its own L2.
+    // Neighbouring channel chunks read the same halo channels, so the ids
+    // are remapped to give each XCD a contiguous run of (image, band, chunk)
+    // with the chunk fastest: the halo is read from HBM once per XCD run.
+    // Ids past the last multiple of 8 keep their position.
+    const int nblk = gridDim.x;
+    const int full = nblk & ~7;
+    const int wg = blockIdx.x;
+    int b = wg < full ? (wg & 7) * (full >> 3) + (wg >> 3) : wg;
     const int chunk = b % p.nchunk;
-    const int n = b / p.nchunk;
+    b /= p.nchunk;
+    const int band = b % p.nband;
+    const int n = b / p.nband;
     const int c0 = chunk * p.CB;
     const int p0 = band * p.PB;
     const int pend = min(p0 + p.PB, p.P);
