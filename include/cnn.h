@@ -212,8 +212,9 @@ int cnn_net_out_shape(const cnn_layer_desc* layers, int n_layers, int N, int C,
  * of the largest intermediate tensor, each 256-byte aligned, plus room for
  * the outputs of the conv and FC layers whose reduction may be split across
  * workgroups (small outputs, e.g. at batch 1; they are set to their biases
- * together at the start of a pass).  The size does not depend on tuning.
- * 0 on error. */
+ * together, by the pooling kernel that runs just before the first of them,
+ * or else by one launch at the start of a pass).  The size does not depend
+ * on tuning.  0 on error. */
 size_t cnn_net_workspace_bytes(const cnn_layer_desc* layers, int n_layers,
                                int N, int C, int H, int W);
 
@@ -235,7 +236,8 @@ int cnn_net_fwd(const cnn_layer_desc* layers, int n_layers, const float* x,
  * time each layer (the paper times whole networks and the heaviest conv
  * layer separately, Sec. 4.2).  A RELU layer executed inside its predecessor,
  * and an LRN layer executed inside the pooling layer after it, get an empty
- * interval. */
+ * interval; the bias fills of split layers count in the interval of the
+ * pooling layer that performs them. */
 int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x,
                       int N, int C, int H, int W, float* y, void* ws,
                       size_t ws_bytes, void* const* events, cnn_stream_t stream);

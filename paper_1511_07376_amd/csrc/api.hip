@@ -298,17 +298,36 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
     int last = n - 1;
     while (last > 0 && plan[last].skipped) --last;
 
-    // Every split-reduction output starts as its bias: one launch for all.
+    // Every split-reduction output starts as its bias.  The pooling kernel
+    // that runs just before the first such layer does the fills after its
+    // own work (no launch of their own); otherwise one launch at the start
+    // of the pass does them all.
+    FillJobs host_fills;
+    host_fills.n = 0;
+    int fill_host = -1;
     {
         std::vector<BiasFill> fills;
+        int first_split = -1;
         for (int i = 0; i < n; ++i) {
             const Plan& p = plan[i];
             if (!p.split || p.skipped) continue;
+            if (first_split < 0) first_split = i;
             float* dst = i == last ? y : reinterpret_cast<float*>(split_area + p.split_off);
             fills.push_back(BiasFill{dst, L[i].bias, N, p.outC, p.outH * p.outW});
         }
-        rc = launch_bias_fills(fills.data(), (int)fills.size(), st);
-        if (rc) return rc;
+        if (!fills.empty() && (int)fills.size() <= kMaxBiasFills) {
+            int h = first_split - 1;
+            while (h >= 0 && plan[h].skipped) --h;
+            if (h >= 0 && plan[h].type == CNN_LAYER_POOL) {
+                fill_host = h;
+                host_fills.n = (int)fills.size();
+                for (int j = 0; j < host_fills.n; ++j) host_fills.job[j] = fills[j];
+            }
+        }
+        if (fill_host < 0) {
+            rc = launch_bias_fills(fills.data(), (int)fills.size(), st);
+            if (rc) return rc;
+        }
     }
 
     const float* cur = x;
@@ -350,15 +369,17 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
                 rc = launch_fc(cur, N, p.inC * p.inH * p.inW, d.weight, d.bias, p.outC, p.relu, out, st,
                                relu_in, relu_left, p.split);
                 break;
-            case CNN_LAYER_POOL:
+            case CNN_LAYER_POOL: {
+                const FillJobs* fj = i == fill_host ? &host_fills : nullptr;
                 if (p.lrn_from >= 0) {  // cur is still the LRN's input
                     const cnn_layer_desc& ld = L[p.lrn_from];
                     rc = launch_lrn_pool(p.pool, d.pool_mode, p.relu, ld.lrn_size, ld.lrn_alpha,
-                                         ld.lrn_beta, ld.lrn_k, cur, out, d.pool_index, st, relu_in);
+                                         ld.lrn_beta, ld.lrn_k, cur, out, d.pool_index, st, relu_in, fj);
                 } else {
-                    rc = launch_pool(p.pool, d.pool_mode, p.relu, cur, out, d.pool_index, st, relu_in);
+                    rc = launch_pool(p.pool, d.pool_mode, p.relu, cur, out, d.pool_index, st, relu_in, fj);
                 }
                 break;
+            }
             case CNN_LAYER_LRN:
                 rc = launch_lrn(cur, N, p.inC, p.inH, p.inW, d.lrn_size, d.lrn_alpha, d.lrn_beta,
                                 d.lrn_k, out, st, relu_in);

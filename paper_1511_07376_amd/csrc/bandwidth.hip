@@ -2,6 +2,7 @@
 // bytes than they compute, so each kernel reads its input once from HBM with
 // consecutive lanes on consecutive addresses and writes its output once.
 #include "common.h"
+#include "fill_jobs.h"
 
 #include <algorithm>
 #include <cmath>
@@ -32,6 +33,7 @@ struct PoolParams {
     int total;  // N*C*P*Q
     int relu;
     int relu_x;  // take the input through a ReLU as it is read
+    FillJobs fills;  // bias fills run after the pooling (n = 0: none)
 };
 
 template <bool WITH_IDX>
@@ -62,6 +64,7 @@ __global__ void __launch_bounds__(kThreads) maxpool_f32(PoolParams p) {
         p.y[o] = best;
         if (WITH_IDX) p.idx[o] = bi;
     }
+    run_fills(p.fills);
 }
 
 // Division by a runtime constant through a multiply-high (exact for n < 2^31).
@@ -148,6 +151,7 @@ pool_staged_f32(PoolParams p, int planes_per_block, int nplanes, FastDiv fpq, Fa
         }
         __syncthreads();
     }
+    run_fills(p.fills);
 }
 
 __global__ void __launch_bounds__(kThreads) avgpool_f32(PoolParams p) {
@@ -171,6 +175,7 @@ __global__ void __launch_bounds__(kThreads) avgpool_f32(PoolParams p) {
         if (p.relu) v = v > 0.0f ? v : 0.0f;
         p.y[o] = v;
     }
+    run_fills(p.fills);
 }
 
 // ------------------------------------------------------------------ LRN
@@ -264,6 +269,7 @@ struct LrnPoolParams {
     FastDiv f_plane, f_w, f_pbq, f_q;  // RB*W, W, PB*Q, Q
     int relu;
     float alpha_over_size, beta, k;
+    FillJobs fills;  // bias fills run after the pooling (n = 0: none)
 };
 
 template <int HALF, int CC, int MODE, bool WITH_IDX>  // MODE 0: max, 1: average
@@ -357,6 +363,7 @@ __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
         if (p.relu) out = out > 0.0f ? out : 0.0f;
         p.y[(size_t)(n * p.C + c0 + c) * PQ + pp * p.Q + q] = out;
     }
+    run_fills(p.fills);
 }
 
 // Any odd size: recompute the clipped window sum for every channel.
@@ -399,9 +406,11 @@ __global__ void __launch_bounds__(kThreads) relu_f32(const float* x, float* y, i
 }  // namespace
 
 int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y, int32_t* idx,
-                hipStream_t st, bool relu_x) {
+                hipStream_t st, bool relu_x, const FillJobs* fills) {
     PoolParams p;
     p.relu_x = relu_x;
+    p.fills.n = 0;
+    if (fills) p.fills = *fills;
     p.x = x;
     p.y = y;
     p.idx = idx;
@@ -409,7 +418,7 @@ int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y
     p.kh = s.kh; p.kw = s.kw; p.sh = s.sh; p.sw = s.sw; p.ph = s.ph; p.pw = s.pw;
     p.total = s.N * s.C * s.P * s.Q;
     p.relu = relu;
-    if (p.total == 0) return CNN_OK;
+    if (p.total == 0) return fills ? launch_bias_fills(fills->job, fills->n, st) : CNN_OK;
     const int plane_bytes = s.H * s.W * 4;
     if (plane_bytes <= kPoolLdsBytes) {
         const int ppb = kPoolLdsBytes / plane_bytes;
@@ -550,8 +559,9 @@ bool lrn_pool_fusable(const PoolShape& s, int size) {
 }
 
 int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alpha, float beta, float k,
-                    const float* x, float* y, int32_t* idx, hipStream_t st, bool relu_x) {
-    if (s.N == 0) return CNN_OK;
+                    const float* x, float* y, int32_t* idx, hipStream_t st, bool relu_x,
+                    const FillJobs* fills) {
+    if (s.N == 0) return fills ? launch_bias_fills(fills->job, fills->n, st) : CNN_OK;
     const int half = size / 2;
     LrnPoolTiling t;
     if (!lrn_pool_fusable(s, size) || !lrn_pool_tiling(s, half, &t))
@@ -576,6 +586,8 @@ int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alph
     p.beta = beta;
     p.k = k;
     p.relu_x = relu_x;
+    p.fills.n = 0;
+    if (fills) p.fills = *fills;
     const size_t shm = (size_t)p.CB * p.RB * s.W * 4;
     const dim3 grid((unsigned)t.blocks), block(kThreads);
 #define CNN_LRN_POOL_CC(H, CC)                                                                   \

@@ -84,9 +84,18 @@ struct BiasFill {
     int N, O, inner;
 };
 int launch_bias_fills(const BiasFill* jobs, int n, hipStream_t st);
+// Up to kMaxBiasFills of them, as a kernel argument: bias_fill_multi runs
+// them on their own, and a pooling kernel runs them after its own work
+// (fills argument of launch_pool / launch_lrn_pool), which saves the network
+// executor a launch.
+struct FillJobs {
+    BiasFill job[kMaxBiasFills];
+    int n;
+};
 // relu_x (pooling, LRN): take the input through a ReLU as it is read.
+// fills: bias fills the kernel also performs (NULL: none).
 int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y, int32_t* idx,
-                hipStream_t st, bool relu_x = false);
+                hipStream_t st, bool relu_x = false, const FillJobs* fills = nullptr);
 int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha, float beta,
                float k, float* y, hipStream_t st, bool relu_x = false);
 int launch_relu(const float* x, float* y, int64_t n, hipStream_t st);
@@ -95,7 +104,8 @@ int launch_relu(const float* x, float* y, int64_t n, hipStream_t st);
 // lrn_pool_fusable() holds.
 bool lrn_pool_fusable(const PoolShape& s, int size);
 int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alpha, float beta, float k,
-                    const float* x, float* y, int32_t* idx, hipStream_t st, bool relu_x = false);
+                    const float* x, float* y, int32_t* idx, hipStream_t st, bool relu_x = false,
+                    const FillJobs* fills = nullptr);
 int launch_softmax(const float* x, int N, int C, int HW, float* y, hipStream_t st);
 
 }  // namespace cnn

@@ -21,6 +21,7 @@
 // pre-filled with the bias, and a ReLU, when the layer has one, runs after the
 // last partial sum has landed.
 #include "common.h"
+#include "fill_jobs.h"
 
 #include <algorithm>
 
@@ -222,22 +223,8 @@ __global__ void fc_fill_bias(float* y, const float* bias, int N, int O) {
         y[i] = bias ? bias[i % O] : 0.0f;
 }
 
-// Several outputs at once: job j sets y_j[n][o][i] = bias_j[o] (or 0) for
-// i < inner.
-struct FillJobs {
-    BiasFill job[kMaxBiasFills];
-    int n;
-};
-
-__global__ void bias_fill_multi(FillJobs f) {
-    for (int j = 0; j < f.n; ++j) {
-        const BiasFill& jb = f.job[j];
-        const int64_t total = (int64_t)jb.N * jb.O * jb.inner;
-        for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-             i += (int64_t)gridDim.x * blockDim.x)
-            jb.y[i] = jb.bias ? jb.bias[(i / jb.inner) % jb.O] : 0.0f;
-    }
-}
+// Several outputs at once (FillJobs).
+__global__ void bias_fill_multi(FillJobs f) { run_fills(f); }
 
 // Tile and reduction split of an FC layer (one rule for launch_fc and the
 // network planner).
