@@ -108,3 +108,23 @@ def test_random_net_matches_oracle(gpu, seed):
         y = to_host(model(to_dev(x)))
         ref = oracle.net_fwd(net, x, params)
         assert_gemm_close(y.reshape(ref.shape), ref, _last_fc_in(net), f"random{seed} B{batch}")
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("seed", range(0, N_NETS, 4))
+def test_random_net_graph_mode(gpu, seed):
+    """The library's graph execution mode (capture once, replay) on random
+    chains: every replay, with new input data in the same buffer, matches the
+    eager network."""
+    net = random_net(seed)
+    params = wl.make_params(net, seed)
+    eager = gpu.Network(net, params)
+    graphed = gpu.Network(net, params, execution_mode="graph")
+    x = to_dev(wl.make_input(net, 5, 200 + seed))
+    for i in range(3):
+        print(f"random net {seed} graph replay {i}", flush=True)
+        x.copy_(to_dev(wl.make_input(net, 5, 300 + seed + i)))
+        y = to_host(graphed(x))
+        ref = to_host(eager(x))
+        assert_gemm_close(y, ref, _last_fc_in(net), f"random{seed} graph replay {i}")
+    graphed.close()
