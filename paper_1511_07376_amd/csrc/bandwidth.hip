@@ -421,8 +421,11 @@ int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y
     if (p.total == 0) return fills ? launch_bias_fills(fills->job, fills->n, st) : CNN_OK;
     const int plane_bytes = s.H * s.W * 4;
     if (plane_bytes <= kPoolLdsBytes) {
-        const int ppb = kPoolLdsBytes / plane_bytes;
+        // planes per workgroup: as many as the staging buffer holds, but no
+        // more than leaves ~2048 workgroups, so that small layers still
+        // spread over every CU
         const int nplanes = s.N * s.C;
+        const int ppb = std::max(1, std::min(kPoolLdsBytes / plane_bytes, nplanes / 2048));
         const dim3 g(std::min(ceil_div(nplanes, ppb), 1 << 20)), b(kThreads);
         const size_t shm = (size_t)ppb * plane_bytes;
         const FastDiv fpq = make_fastdiv(s.P * s.Q), fq = make_fastdiv(s.Q);
