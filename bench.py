@@ -114,11 +114,17 @@ def cpu_baseline(net, x, params, budget_s):
     t1 = time.perf_counter() - t0
     n_more = int(max(0, min(x.shape[0] - 1, (budget_s - t1) / max(t1, 1e-3))))
     t2 = 0.0
+    reps = 0
+    n = 1
     if n_more > 0:
-        t0 = time.perf_counter()
-        oracle.net_fwd(net, x[1:1 + n_more], params)
-        t2 = time.perf_counter() - t0
-    n = 1 + n_more
+        # the same images again while less than ~2/3 of the budget is spent,
+        # so that a fast oracle pass is still timed over several seconds
+        while reps == 0 or (t1 + t2 < 0.67 * budget_s and reps < 10000):
+            t0 = time.perf_counter()
+            oracle.net_fwd(net, x[1:1 + n_more], params)
+            t2 += time.perf_counter() - t0
+            reps += 1
+        n = 1 + reps * n_more
     # the paper's sequential baseline: one thread, one image
     oracle.set_threads(1)
     t0 = time.perf_counter()
@@ -126,9 +132,9 @@ def cpu_baseline(net, x, params, budget_s):
     t_one = time.perf_counter() - t0
     oracle.set_threads(threads)
     return {"value": n / (t1 + t2), "unit": "images/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n} of the {x.shape[0]} images of the same batch through the oracle's "
-                      f"layer-by-layer network (double accumulation, OpenMP over images x "
-                      f"channels), {t1 + t2:.1f} s",
+            "sample": f"{n} images ({max(reps, 1)} pass(es) over {1 + n_more} of the {x.shape[0]} images of "
+                      f"the same batch) through the oracle's layer-by-layer network (double "
+                      f"accumulation, OpenMP over images x channels), {t1 + t2:.1f} s",
             "value_1_thread": round(1.0 / t_one, 3)}
 
 
