@@ -241,8 +241,12 @@ FcGeom fc_geom(int N) {
 // Splits and the reduction length per split.
 int fc_split(const FcGeom& g, int N, int I, int O, int* kchunk) {
     const int tiles = ceil_div(N, g.tm) * ceil_div(O, g.tn);
-    // enough splits to reach the target, but at least one round per split
-    int splits = std::min(ceil_div(g.target, tiles), std::max(1, I / g.unit));
+    // Enough splits to reach the target, with at least one ring round per
+    // split; with 64-image tiles at least four, since there a layer with few
+    // output tiles (AlexNet's fc8 at batch 64: 16) is bound by its atomic
+    // partial sums rather than by its weight stream (fc8 18 -> 15 us).
+    const int min_rounds = g.tm == 64 ? 4 : 1;
+    int splits = std::min(ceil_div(g.target, tiles), std::max(1, I / (min_rounds * g.unit)));
     splits = std::max(splits, 1);
     *kchunk = ceil_div(ceil_div(I, splits), g.unit) * g.unit;
     return ceil_div(I, *kchunk);
