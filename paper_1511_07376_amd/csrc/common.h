@@ -73,6 +73,8 @@ int launch_fc(const float* x, int N, int I, const float* w, const float* bias, i
               bool prefilled = false);
 // Reduction splits launch_fc uses for this shape; above 1 its output must
 // start as the bias (launch_fc fills it unless told it is prefilled).
+// Batches of at most kGemvMaxN images take an unsplit matrix-vector kernel.
+constexpr int kGemvMaxN = 2;
 int fc_splits(int N, int I, int O);
 // y_j[n][o][i] = bias_j[o] (or 0), i < inner, for several layer outputs
 // (FC: inner = 1; conv NCHW: inner = P*Q), in one launch per kMaxBiasFills

@@ -24,6 +24,7 @@
 #include "fill_jobs.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace cnn {
 namespace {
@@ -223,6 +224,113 @@ __global__ void fc_fill_bias(float* y, const float* bias, int N, int O) {
         y[i] = bias ? bias[i % O] : 0.0f;
 }
 
+// Batches of at most kGemvMaxN images: a matrix-vector product per image on
+// the vector ALUs, since a 32-row MFMA tile would be mostly empty.  A
+// workgroup owns R consecutive output features (4, or 1 when there are fewer
+// than 4096 of them, so that the launch still has ~1000 workgroups) and its
+// four waves take a quarter of the reduction each.  A lane streams the weight
+// rows with 128-bit loads (VEC; 32-bit otherwise), four steps in flight,
+// multiplies them by the images' inputs (served from L2), and the partial
+// sums are reduced across the wave and then through LDS across the four
+// waves.  The bias and the ReLU are applied as the sum is stored: no split,
+// no bias fill and no atomics, so the result is the same from run to run.
+template <int N, int R, bool VEC, bool RELU_X>
+__global__ void __launch_bounds__(256) fc_gemv_f32(FcParams p) {
+    typedef typename std::conditional<VEC, float4, float>::type V;
+    constexpr int W = VEC ? 4 : 1;                   // floats per load
+    constexpr int U = 4;                             // steps in flight
+    __shared__ float part[4][R][N];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int o0 = blockIdx.x * R;
+    const int KV = p.I / W;                          // loads per row
+    const int per = (KV + 3) / 4;                    // this wave's range
+    const int kb = wave * per, ke = min(KV, kb + per);
+    const V* wr[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        wr[r] = reinterpret_cast<const V*>(p.w + (size_t)min(o0 + r, p.O - 1) * p.I);
+    const V* xr = reinterpret_cast<const V*>(p.x);
+    auto dot = [](const V& a, const V& b) -> float {
+        if constexpr (VEC) return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+        else return a * b;
+    };
+    auto relu_v = [](V v) -> V {
+        if constexpr (!RELU_X) return v;
+        else if constexpr (VEC) return make_float4(fmaxf(v.x, 0.0f), fmaxf(v.y, 0.0f), fmaxf(v.z, 0.0f), fmaxf(v.w, 0.0f));
+        else return fmaxf(v, 0.0f);
+    };
+    float acc[R][N];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int n = 0; n < N; ++n) acc[r][n] = 0.0f;
+    int k = kb + lane;
+    for (; k + (U - 1) * 64 < ke; k += U * 64) {
+        V wv[U][R], xv[U][N];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int r = 0; r < R; ++r) wv[u][r] = wr[r][k + u * 64];
+#pragma unroll
+            for (int n = 0; n < N; ++n) xv[u][n] = relu_v(xr[(size_t)n * KV + k + u * 64]);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int n = 0; n < N; ++n) acc[r][n] += dot(wv[u][r], xv[u][n]);
+    }
+    for (; k < ke; k += 64) {
+#pragma unroll
+        for (int n = 0; n < N; ++n) {
+            const V xv = relu_v(xr[(size_t)n * KV + k]);
+#pragma unroll
+            for (int r = 0; r < R; ++r) acc[r][n] += dot(wr[r][k], xv);
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int n = 0; n < N; ++n) {
+            float v = acc[r][n];
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+            if (lane == 0) part[wave][r][n] = v;
+        }
+    __syncthreads();
+    const int t = threadIdx.x;
+    if (t < R * N) {
+        const int r = t / N, n = t - r * N;
+        const int o = o0 + r;
+        if (o < p.O) {
+            float v = (part[0][r][n] + part[1][r][n]) + (part[2][r][n] + part[3][r][n]);
+            if (p.bias) v += p.bias[o];
+            if (p.relu) v = v > 0.0f ? v : 0.0f;
+            p.y[(size_t)n * p.O + o] = v;
+        }
+    }
+}
+
+template <int N, int R>
+int launch_fc_gemv_r(const FcParams& prm, bool vec, bool relu_in, hipStream_t st) {
+    const dim3 grid(ceil_div(prm.O, R)), block(256);
+    if (vec) {
+        if (relu_in) hipLaunchKernelGGL((fc_gemv_f32<N, R, true, true>), grid, block, 0, st, prm);
+        else hipLaunchKernelGGL((fc_gemv_f32<N, R, true, false>), grid, block, 0, st, prm);
+    } else {
+        if (relu_in) hipLaunchKernelGGL((fc_gemv_f32<N, R, false, true>), grid, block, 0, st, prm);
+        else hipLaunchKernelGGL((fc_gemv_f32<N, R, false, false>), grid, block, 0, st, prm);
+    }
+    return check_launch("fc_gemv_f32");
+}
+
+template <int N>
+int launch_fc_gemv(const FcParams& prm, bool vec, bool relu_in, hipStream_t st) {
+    return prm.O >= 4096 ? launch_fc_gemv_r<N, 4>(prm, vec, relu_in, st)
+                         : launch_fc_gemv_r<N, 1>(prm, vec, relu_in, st);
+}
+
 // Several outputs at once (FillJobs).
 __global__ void bias_fill_multi(FillJobs f) { run_fills(f); }
 
@@ -286,7 +394,7 @@ int launch_fc_cfg(const FcParams& prm0, const FcGeom& g, hipStream_t st, bool* r
 
 int fc_splits(int N, int I, int O) {
     int kchunk;
-    return N > 0 ? fc_split(fc_geom(N), N, I, O, &kchunk) : 1;
+    return N > 0 && N > kGemvMaxN ? fc_split(fc_geom(N), N, I, O, &kchunk) : 1;
 }
 
 int launch_bias_fills(const BiasFill* jobs, int n, hipStream_t st) {
@@ -326,6 +434,10 @@ int launch_fc(const float* x, int N, int I, const float* w, const float* bias, i
     prm.relu = relu;
     const bool vec = (I % 4 == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0) &&
                      ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
+    if (N <= kGemvMaxN) {  // unsplit: the output needs no fill and the ReLU is applied here
+        static_assert(kGemvMaxN == 2, "one instantiation per batch size");
+        return N == 1 ? launch_fc_gemv<1>(prm, vec, relu_in, st) : launch_fc_gemv<2>(prm, vec, relu_in, st);
+    }
     const FcGeom g = fc_geom(N);
 #define CNN_FC_CFG(WMW, WNW, FM, FN, BK, D)                                                                  \
     (vec ? (relu_in ? launch_fc_cfg<WMW, WNW, FM, FN, BK, D, true, true>(prm, g, st, relu_left, prefilled)    \

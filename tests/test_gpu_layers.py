@@ -141,6 +141,12 @@ FC_CASES = [
     # k-streaming kernel (batches up to 64, inputs a multiple of 4): 1 to 4 row
     # blocks of 16, with and without the reduction split over workgroups
     (48, 512, 300, True, None), (20, 3072, 4100, True, [0, 7, 19]), (64, 96, 17, False, None),
+    # batches of 1 and 2: the matrix-vector kernel (128-bit and 32-bit loads,
+    # 4-row and 1-row workgroups, a ragged last workgroup); 3 and 4 images on
+    # the matrix cores next to them
+    (1, 9216, 4096, True, None), (2, 4096, 1000, False, None), (2, 4100, 4098, True, [0, 1]),
+    (1, 4096, 4101, False, None), (4, 1024, 33, True, None), (4, 100, 7, False, None),
+    (2, 1001, 13, True, None),
 ]
 
 
@@ -157,17 +163,18 @@ def test_fc(gpu, case):
     assert_gemm_close(yg[rows], oracle.fc_fwd(x[rows], w, b, relu), I, tag)
 
 
-def test_fc_unaligned_and_no_bias(gpu):
-    x = wl.normal((7 * 96 + 1,), 1.0, 8, 0)
+@pytest.mark.parametrize("N", [7, 2])
+def test_fc_unaligned_and_no_bias(gpu, N):
+    x = wl.normal((N * 96 + 1,), 1.0, 8, 0)
     w = wl.normal((40, 96), 1.0, 8, 1)
     xd = to_dev(x)[1:]                     # 4-byte offset: not 16-byte aligned
-    ref_in = x[1:].reshape(7, 96)
+    ref_in = x[1:].reshape(N, 96)
     # unaligned pointer through the raw ABI
-    y = torch.empty((7, 40), device="cuda")
-    rc = gpu.lib.cnn_fc_fwd(xd.data_ptr(), 7, 96, to_dev(w).data_ptr(), None, 40, 0, y.data_ptr(),
+    y = torch.empty((N, 40), device="cuda")
+    rc = gpu.lib.cnn_fc_fwd(xd.data_ptr(), N, 96, to_dev(w).data_ptr(), None, 40, 0, y.data_ptr(),
                             torch.cuda.current_stream().cuda_stream)
     assert rc == 0, gpu.cnn_last_error()
-    assert_gemm_close(to_host(y), oracle.fc_fwd(ref_in, w, None), 96, "fc unaligned")
+    assert_gemm_close(to_host(y), oracle.fc_fwd(ref_in, w, None), 96, f"fc unaligned N{N}")
 
 
 # ---------------------------------------------------------------- pooling
