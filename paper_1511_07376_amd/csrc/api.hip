@@ -31,23 +31,28 @@ int check_launch(const char* what) {
     return CNN_OK;
 }
 
+// Output extents are computed in 64 bits (a padding near INT_MAX must not
+// wrap) and must fit an int.
 int conv_out(int H, int W, int R, int S, int sh, int sw, int ph, int pw, int* P, int* Q) {
     if (H <= 0 || W <= 0) return fail(CNN_ERR_INVALID, "conv: input %dx%d is empty", H, W);
     if (R <= 0 || S <= 0) return fail(CNN_ERR_INVALID, "conv: kernel %dx%d", R, S);
     if (sh <= 0 || sw <= 0) return fail(CNN_ERR_INVALID, "conv: stride %dx%d", sh, sw);
     if (ph < 0 || pw < 0) return fail(CNN_ERR_INVALID, "conv: negative padding");
-    if (H + 2 * ph < R || W + 2 * pw < S)
-        return fail(CNN_ERR_INVALID, "conv: kernel %dx%d larger than padded input %dx%d", R, S,
-                    H + 2 * ph, W + 2 * pw);
-    *P = (H + 2 * ph - R) / sh + 1;
-    *Q = (W + 2 * pw - S) / sw + 1;
+    const int64_t hp = (int64_t)H + 2 * (int64_t)ph, wp = (int64_t)W + 2 * (int64_t)pw;
+    if (hp < R || wp < S)
+        return fail(CNN_ERR_INVALID, "conv: kernel %dx%d larger than padded input %lldx%lld", R, S,
+                    (long long)hp, (long long)wp);
+    const int64_t p = (hp - R) / sh + 1, q = (wp - S) / sw + 1;
+    if (p > INT32_MAX || q > INT32_MAX) return fail(CNN_ERR_UNSUPPORTED, "conv: output extent too large");
+    *P = (int)p;
+    *Q = (int)q;
     return CNN_OK;
 }
 
 namespace {
-int pool_extent(int in, int k, int s, int pad, int ceil_mode) {
-    const int span = in + 2 * pad - k;
-    int out = ceil_mode ? (span + s - 1) / s + 1 : span / s + 1;
+int64_t pool_extent(int64_t in, int64_t k, int64_t s, int64_t pad, int ceil_mode) {
+    const int64_t span = in + 2 * pad - k;
+    int64_t out = ceil_mode ? (span + s - 1) / s + 1 : span / s + 1;
     if (ceil_mode && (out - 1) * s >= in + pad) --out;  // window would start past the image
     return out;
 }
@@ -61,10 +66,12 @@ int pool_out(int H, int W, int kh, int kw, int sh, int sw, int ph, int pw, int c
     if (ph < 0 || pw < 0 || ph >= kh || pw >= kw)
         return fail(CNN_ERR_INVALID, "pool: padding %dx%d must be >= 0 and below the window %dx%d",
                     ph, pw, kh, kw);
-    if (H + 2 * ph < kh || W + 2 * pw < kw)
+    if ((int64_t)H + 2 * (int64_t)ph < kh || (int64_t)W + 2 * (int64_t)pw < kw)
         return fail(CNN_ERR_INVALID, "pool: window larger than padded input");
-    *P = pool_extent(H, kh, sh, ph, ceil_mode);
-    *Q = pool_extent(W, kw, sw, pw, ceil_mode);
+    const int64_t p = pool_extent(H, kh, sh, ph, ceil_mode), q = pool_extent(W, kw, sw, pw, ceil_mode);
+    if (p > INT32_MAX || q > INT32_MAX) return fail(CNN_ERR_UNSUPPORTED, "pool: output extent too large");
+    *P = (int)p;
+    *Q = (int)q;
     return CNN_OK;
 }
 

@@ -53,6 +53,20 @@ def test_conv_out_shape_agrees_with_oracle(H, R, s, p):
         oracle.conv2d_out_shape(H, H + 3, R, R, s, s, p, p)
 
 
+def test_shape_arithmetic_near_int_max():
+    """Extents near INT32_MAX are computed without wrapping: an output that
+    does not fit is rejected, one that does is exact."""
+    big = 2**31 - 1
+    with pytest.raises(cnn.CnnError):
+        cnn.cnn_conv2d_out_shape(1, 1, 1, 1, 1, big)          # 1 + 2*pad output rows
+    assert cnn.cnn_conv2d_out_shape(big, 1, big, 1, 1, 0) == (1, 1)
+    e = (big + 2 * 2**30 - 3) // 2**30 + 1                    # exact, 64-bit
+    assert cnn.cnn_conv2d_out_shape(big, big, 3, 3, 2**30, 2**30) == (e, e)
+    with pytest.raises(cnn.CnnError):
+        cnn.cnn_pool_out_shape(big, 1, (2, 1), 1, (1, 0))      # 2^31 windows
+    assert cnn.cnn_pool_out_shape(big, big, big, big, 0, True) == (1, 1)
+
+
 def test_pool_out_shape_agrees_with_oracle_exhaustive():
     for H in range(1, 20):
         for k in range(1, 5):
