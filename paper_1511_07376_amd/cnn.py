@@ -117,7 +117,8 @@ class CnnError(RuntimeError):
 
 
 def cnn_last_error() -> str:
-    return lib.cnn_last_error().decode()
+    # the message may quote the caller's text (a NetFile line), which need not be UTF-8
+    return lib.cnn_last_error().decode(errors="replace")
 
 
 def cnn_version() -> str:
