@@ -180,6 +180,82 @@ def conv_sweep(args):
     cnn.cnn_set_autotune(False)
 
 
+def conv_shapes(net, batch, cnn):
+    """(name, N, C, H, W, layer) for each conv layer, with the library's shape rules."""
+    c, h, w = net.input_chw
+    out, nconv = [], 0
+    for layer in net.layers:
+        if layer.kind == "conv":
+            nconv += 1
+            out.append((f"conv{nconv}", batch, c, h, w, layer))
+            h, w = cnn.cnn_conv2d_out_shape(h, w, *layer.kernel, layer.stride, layer.pad)
+            c = layer.out_channels
+        elif layer.kind == "pool":
+            h, w = cnn.cnn_pool_out_shape(h, w, layer.kernel, layer.stride, layer.pad, layer.ceil)
+        elif layer.kind == "fc":
+            c, h, w = layer.out_features, 1, 1
+    return out
+
+
+def gemm_reference(args):
+    """Each conv layer of the network beside torch's fp32 batched GEMM on the
+    same contraction with the im2col matrix already unrolled in memory (so the
+    library pays no gather): per group, [K/G x (C/G)RS] times [(C/G)RS x NPQ],
+    and the pixel-major [NPQ x (C/G)RS] times its transpose.  Context for the
+    implicit-GEMM kernels, one JSON line per layer."""
+    import torch
+    from paper_1511_07376_amd import cnn
+    from paper_1511_07376_amd import workloads as wl
+
+    torch.backends.cuda.matmul.allow_tf32 = False
+    net = wl.NETS[args.net]
+    batch = args.batch or (64 if args.net == "alexnet" else net.default_batch)
+    cnn.cnn_set_autotune(True)
+
+    def timed(fn):
+        for _ in range(max(args.warmup, 1)):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    for name, n, c, h, w_, layer in conv_shapes(net, batch, cnn):
+        g, (r, s_) = layer.groups, layer.kernel
+        k = layer.out_channels
+        p, q = cnn.cnn_conv2d_out_shape(h, w_, r, s_, layer.stride, layer.pad)
+        kg, kr, m = k // g, (c // g) * r * s_, n * p * q
+        flops = 2.0 * g * kg * kr * m
+        x = torch.rand(n, c, h, w_, device="cuda")
+        wt = torch.randn(k, c // g, r, s_, device="cuda") * 0.05
+        b = torch.randn(k, device="cuda")
+        y = torch.empty(n, k, p, q, device="cuda")
+        ms_ours = timed(lambda: cnn.cnn_conv2d_fwd(x, wt, b, layer.stride, layer.pad, g, True, y=y))
+        del x, y
+        a = torch.randn(g, kg, kr, device="cuda")
+        bm = torch.randn(g, kr, m, device="cuda")
+        ms_km = timed(lambda: torch.bmm(a, bm))
+        del bm
+        xm = torch.randn(g, m, kr, device="cuda")
+        at = a.transpose(1, 2).contiguous()
+        ms_mk = timed(lambda: torch.bmm(xm, at))
+        del xm
+        rec = {"layer": name, "gemm": {"groups": g, "rows": kg, "reduction": kr, "cols": m},
+               "implicit_gemm_us": round(ms_ours * 1e3, 1),
+               "library_gemm_us": {"channels_x_pixels": round(ms_km * 1e3, 1),
+                                   "pixels_x_channels": round(ms_mk * 1e3, 1)},
+               "frac_fp32_mfma": {"implicit_gemm": round(flops / ms_ours / 1e9 / PEAK_FP32_MFMA_TFLOPS, 3),
+                                  "library_best": round(flops / min(ms_km, ms_mk) / 1e9
+                                                        / PEAK_FP32_MFMA_TFLOPS, 3)}}
+        print(json.dumps(rec), flush=True)
+        torch.cuda.empty_cache()
+    cnn.cnn_set_autotune(False)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -205,6 +281,9 @@ def main():
                          "batches 1, 16, 64, bias + ReLU fused), one JSON line per case")
     ap.add_argument("--sweep-miopen", action="store_true",
                     help="with --sweep: also time torch's own conv2d (MIOpen) on the same tensors, as context")
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="instead of the network: time each conv layer beside torch's fp32 batched GEMM "
+                         "on its contraction with the im2col matrix precomputed, one JSON line per layer")
     args = ap.parse_args()
     if args.copy_probe:
         import torch
@@ -216,6 +295,8 @@ def main():
         return
     if args.sweep:
         return conv_sweep(args)
+    if args.gemm_reference:
+        return gemm_reference(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the images of a batch are independent: on N GPUs each would run batch/N)",

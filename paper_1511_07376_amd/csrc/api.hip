@@ -110,7 +110,8 @@ int check_pool(int N, int C, int H, int W, int mode, int kh, int kw, int sh, int
     int P, Q;
     int rc = pool_out(H, W, kh, kw, sh, sw, ph, pw, ceil_mode, &P, &Q);
     if (rc) return rc;
-    if (too_big(N, C, H, W)) return fail(CNN_ERR_UNSUPPORTED, "pool: tensor exceeds 2^31-1 elements");
+    if (too_big(N, C, H, W) || too_big(N, C, P, Q))  // padding can make the output the larger
+        return fail(CNN_ERR_UNSUPPORTED, "pool: tensor exceeds 2^31-1 elements");
     *s = PoolShape{N, C, H, W, kh, kw, sh, sw, ph, pw, P, Q};
     return CNN_OK;
 }

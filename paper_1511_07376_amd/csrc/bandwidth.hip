@@ -38,7 +38,10 @@ struct PoolParams {
 
 template <bool WITH_IDX>
 __global__ void __launch_bounds__(kThreads) maxpool_f32(PoolParams p) {
-    for (int o = blockIdx.x * kThreads + threadIdx.x; o < p.total; o += gridDim.x * kThreads) {
+    // 64-bit loop counter: the last step past a total near 2^31 must not wrap
+    for (int64_t o64 = blockIdx.x * kThreads + threadIdx.x; o64 < p.total;
+         o64 += (int64_t)gridDim.x * kThreads) {
+        const int o = (int)o64;
         const int q = o % p.Q;
         const int t = o / p.Q;
         const int pp = t % p.P;
@@ -94,7 +97,9 @@ pool_staged_f32(PoolParams p, int planes_per_block, int nplanes, FastDiv fpq, Fa
     const int kh = KH ? KH : p.kh, kw = KW ? KW : p.kw;
     const int sh = KH ? SH : p.sh, sw = KW ? SW : p.sw;
     const int HW = p.H * p.W, PQ = p.P * p.Q;
-    for (int pl0 = blockIdx.x * planes_per_block; pl0 < nplanes; pl0 += gridDim.x * planes_per_block) {
+    for (int64_t pl64 = (int64_t)blockIdx.x * planes_per_block; pl64 < nplanes;
+         pl64 += (int64_t)gridDim.x * planes_per_block) {
+        const int pl0 = (int)pl64;
         const int np = min(planes_per_block, nplanes - pl0);
         const int len = np * HW;
         {  // len <= 16 * kThreads: every load of the run is in flight at once.
@@ -155,7 +160,9 @@ pool_staged_f32(PoolParams p, int planes_per_block, int nplanes, FastDiv fpq, Fa
 }
 
 __global__ void __launch_bounds__(kThreads) avgpool_f32(PoolParams p) {
-    for (int o = blockIdx.x * kThreads + threadIdx.x; o < p.total; o += gridDim.x * kThreads) {
+    for (int64_t o64 = blockIdx.x * kThreads + threadIdx.x; o64 < p.total;
+         o64 += (int64_t)gridDim.x * kThreads) {
+        const int o = (int)o64;
         const int q = o % p.Q;
         const int t = o / p.Q;
         const int pp = t % p.P;
@@ -223,7 +230,9 @@ __global__ void __launch_bounds__(kThreads) lrn_across_f32(LrnParams p) {
     // the NV loads carry no branch, so all of them are in flight at once.
     const __amdgpu_buffer_rsrc_t xres =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.x), (short)0, 0x7fffffff, 0x00020000);
-    for (int t = blockIdx.x * kThreads + threadIdx.x; t < p.total; t += gridDim.x * kThreads) {
+    for (int64_t t64 = blockIdx.x * kThreads + threadIdx.x; t64 < p.total;
+         t64 += (int64_t)gridDim.x * kThreads) {
+        const int t = (int)t64;
         const int hw = t % p.HW;
         const int rest = t / p.HW;
         const int chunk = rest % p.nchunk;
@@ -368,7 +377,9 @@ __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
 
 // Any odd size: recompute the clipped window sum for every channel.
 __global__ void __launch_bounds__(kThreads) lrn_across_any_f32(LrnParams p, int half) {
-    for (int t = blockIdx.x * kThreads + threadIdx.x; t < p.total; t += gridDim.x * kThreads) {
+    for (int64_t t64 = blockIdx.x * kThreads + threadIdx.x; t64 < p.total;
+         t64 += (int64_t)gridDim.x * kThreads) {
+        const int t = (int)t64;
         const int n = t / p.HW;
         const int hw = t - n * p.HW;
         const float* xp = p.x + n * p.C * p.HW + hw;

@@ -219,8 +219,8 @@ fc_gemm_f32(FcParams p) {
 
 // y[n][o] = bias[o] (or 0): the starting value of the split-reduction sums.
 __global__ void fc_fill_bias(float* y, const float* bias, int N, int O) {
-    const int total = N * O;
-    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x)
+    const int64_t total = (int64_t)N * O;
+    for (int64_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x)
         y[i] = bias ? bias[i % O] : 0.0f;
 }
 

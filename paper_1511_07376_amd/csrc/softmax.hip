@@ -36,13 +36,14 @@ __global__ void __launch_bounds__(kThreads) softmax_rows_f32(const float* x, flo
     if (row >= rows) return;
     const float* xr = x + (size_t)row * C;
     float* yr = y + (size_t)row * C;
+    // 64-bit channel counters: a row may hold up to 2^31-1 values
     float m = -INFINITY;
-    for (int c = lane; c < C; c += 64) m = fmaxf(m, xr[c]);
+    for (int64_t c = lane; c < C; c += 64) m = fmaxf(m, xr[c]);
     m = wave_max(m);
     float s = 0.0f;
-    for (int c = lane; c < C; c += 64) s += expf(xr[c] - m);
+    for (int64_t c = lane; c < C; c += 64) s += expf(xr[c] - m);
     s = wave_sum(s);
-    for (int c = lane; c < C; c += 64) yr[c] = expf(xr[c] - m) / s;
+    for (int64_t c = lane; c < C; c += 64) yr[c] = expf(xr[c] - m) / s;
 }
 
 // HW > 1: one thread per (n, i) column, lanes on consecutive positions i of

@@ -166,6 +166,9 @@ def test_fc_pool_lrn_relu_reject():
     assert L.cnn_pool_fwd(FAKE, 1, 1, 8, 8, 0, 2, 2, 2, 2, 2, 0, 1, 0, FAKE, 0, 0) == cnn.CNN_ERR_INVALID
     assert L.cnn_pool_fwd(FAKE, 1, 1, 8, 8, 1, 2, 2, 2, 2, 0, 0, 1, 0, FAKE, FAKE, 0) == cnn.CNN_ERR_INVALID
     assert L.cnn_pool_fwd(FAKE, 1, 1, 8, 8, 7, 2, 2, 2, 2, 0, 0, 1, 0, FAKE, 0, 0) == cnn.CNN_ERR_INVALID
+    # input within 2^31-1 elements (46340^2), padded 2x2/1 output not (46341^2)
+    assert L.cnn_pool_fwd(FAKE, 1, 1, 46340, 46340, 0, 2, 2, 1, 1, 1, 1, 1, 0, FAKE, 0, 0) == \
+        cnn.CNN_ERR_UNSUPPORTED
     assert L.cnn_lrn_fwd(FAKE, 1, 4, 4, 4, 4, 1e-4, 0.75, 1.0, FAKE, 0) == cnn.CNN_ERR_UNSUPPORTED
     assert L.cnn_lrn_fwd(FAKE, 1, 4, 4, 4, 0, 1e-4, 0.75, 1.0, FAKE, 0) == cnn.CNN_ERR_INVALID
     assert L.cnn_relu_fwd(FAKE, FAKE, -1, 0) == cnn.CNN_ERR_INVALID
