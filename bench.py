@@ -281,6 +281,10 @@ def main():
                          "batches 1, 16, 64, bias + ReLU fused), one JSON line per case")
     ap.add_argument("--sweep-miopen", action="store_true",
                     help="with --sweep: also time torch's own conv2d (MIOpen) on the same tensors, as context")
+    ap.add_argument("--streams", type=int, default=1,
+                    help="run the timed steps round-robin on this many streams, each with its own replica "
+                         "of the network (own workspace), so that consecutive passes overlap: serving "
+                         "throughput rather than one pass after another")
     ap.add_argument("--gemm-reference", action="store_true",
                     help="instead of the network: time each conv layer beside torch's fp32 batched GEMM "
                          "on its contraction with the im2col matrix precomputed, one JSON line per layer")
@@ -346,15 +350,39 @@ def main():
         torch.cuda.synchronize()
 
     # timed region: K steps of cnn_net_fwd (graph launches with --graph)
-    torch.cuda.synchronize()
-    start.record()
-    for k in range(args.steps):
-        if graph is not None:
-            graph(xd, y=yd)
-        else:
-            model(xd, y=yd)
-    end.record()
-    torch.cuda.synchronize()
+    if args.streams > 1 and graph is None:
+        # round-robin over replicas on their own streams (default priority);
+        # the start and end events on the current stream bracket them all
+        reps = [model] + [model.replica() for _ in range(args.streams - 1)]
+        ys = [yd] + [torch.empty_like(yd) for _ in range(args.streams - 1)]
+        streams = [torch.cuda.Stream() for _ in range(args.streams)]
+        for _ in range(max(args.warmup, 1)):  # first use of each stream and workspace untimed
+            for j in range(args.streams):
+                reps[j](xd, y=ys[j], stream=streams[j])
+        torch.cuda.synchronize()
+        cur = torch.cuda.current_stream()
+        start.record(cur)
+        for s_ in streams:
+            s_.wait_event(start)
+        for k in range(args.steps):
+            j = k % args.streams
+            reps[j](xd, y=ys[j], stream=streams[j])
+        for s_ in streams:
+            cur.wait_stream(s_)
+        end.record(cur)
+        torch.cuda.synchronize()
+        for j in range(1, args.streams):
+            assert torch.allclose(ys[j], yd, rtol=1e-5, atol=1e-6), "replicas disagree"
+    else:
+        torch.cuda.synchronize()
+        start.record()
+        for k in range(args.steps):
+            if graph is not None:
+                graph(xd, y=yd)
+            else:
+                model(xd, y=yd)
+        end.record()
+        torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / args.steps
     # per-layer region: K more steps with HIP events recorded on the launch
     # stream between the layers (cnn_net_fwd_timed); the event records add a
@@ -428,6 +456,7 @@ def main():
         "ms_per_step_with_layer_events": round(ms_step_events, 4),
         "ms_per_step_with_layer_events_median": round(float(np.median(step_ms_events)), 4),
         "graph_replay": bool(graph is not None),
+        "streams": args.streams,
         "autotune": bool(args.autotune),
         "conv_configs": {" ".join(l.split()[:-1]): cnn.cnn_conv2d_config_name(int(l.split()[-1]))
                          for l in cnn.cnn_tuning_export().splitlines()},

@@ -429,6 +429,23 @@ class Network:
         self._ws: Optional[torch.Tensor] = None
         self._ws_key = None
 
+    def replica(self) -> "Network":
+        """A Network over the same device parameters with its own workspace,
+        index buffers and graphs, so that a second pass can run concurrently
+        on another stream (two passes never share a workspace)."""
+        r = Network.__new__(Network)
+        r.execution_mode = self.execution_mode
+        r._graphs, r._outs = {}, {}
+        r.net, r.device, r.weights = self.net, self.device, self.weights
+        r.pool_index = self.pool_index
+        r.indices = [None] * len(self.net.layers)
+        r.descs = (cnn_layer_desc * len(self.descs))()
+        ctypes.memmove(r.descs, self.descs, ctypes.sizeof(self.descs))
+        for d in r.descs:
+            d.pool_index = None
+        r._ws, r._ws_key = None, None
+        return r
+
     def out_shape(self, N: int) -> Tuple[int, int, int, int]:
         C, H, W = self.net.input_chw
         oc, oh, ow = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()

@@ -239,3 +239,30 @@ def test_workspace_size_does_not_depend_on_tuning(gpu):
     finally:
         gpu.cnn_set_autotune(False)
         gpu.cnn_tuning_clear()
+
+
+def test_replicas_run_concurrently_on_two_streams(gpu):
+    """Network.replica shares the device parameters but not the workspace:
+    passes of the two on two streams, in flight together, each match the
+    oracle on their own input (with indices for the max-pooling layers)."""
+    net = wl.lenet
+    params = wl.make_params(net, 14)
+    model = gpu.Network(net, params, pool_index=True)
+    rep = model.replica()
+    assert rep.weights is model.weights
+    xs = [wl.make_input(net, 16, 14), wl.make_input(net, 16, 15)]
+    xd = [to_dev(x) for x in xs]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    ys = [None, None]
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for j, m in enumerate((model, rep)):
+            with torch.cuda.stream(streams[j]):
+                ys[j] = m(xd[j], stream=streams[j])
+    torch.cuda.synchronize()
+    for j, m in enumerate((model, rep)):
+        ref, ref_idx = oracle.net_fwd(net, xs[j], params, pool_index=True)
+        assert_gemm_close(to_host(ys[j]), ref, net.layers[-1].in_features, f"replica {j}")
+        for i, layer in enumerate(net.layers):
+            if layer.kind == "pool" and layer.mode == "max":
+                assert np.mean(to_host(m.indices[i]) == ref_idx[i]) > 0.999
