@@ -147,6 +147,8 @@ struct Plan {
     bool skipped;          // a RELU layer folded into its predecessor, or an LRN
                            // layer run inside the pooling layer after it
     int lrn_from;          // POOL: index of the LRN layer it runs first, or -1
+    int opad_h, opad_w;    // POOL run with its LRN: the zero border its output
+                           // planes get for the padded conv that reads them
     bool may_split;        // CONV, FC: some configuration splits the reduction
                            // across workgroups (room is kept for the output)
     bool split;            // ... and the one the launch will use does (the
@@ -191,6 +193,25 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
                 rc = check_conv(N, c, h, w, d.out_channels, d.kernel_h, d.kernel_w, d.stride_h,
                                 d.stride_w, d.pad_h, d.pad_w, d.groups, &p.conv);
                 if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
+                // After an LRN + pooling kernel, the padding is written by that
+                // kernel as a zero border around its output planes, and the
+                // conv runs unpadded on the bordered planes: the gather then
+                // needs no per-element padding test (3-5% on AlexNet's conv2
+                // and conv3).
+                if ((d.pad_h > 0 || d.pad_w > 0) && prev_exec >= 0 && plan[prev_exec].type == CNN_LAYER_POOL &&
+                    plan[prev_exec].lrn_from >= 0) {
+                    ConvShape bordered;
+                    const int hb = h + 2 * d.pad_h, wb = w + 2 * d.pad_w;
+                    if (hb > h && wb > w &&
+                        check_conv(N, c, hb, wb, d.out_channels, d.kernel_h, d.kernel_w, d.stride_h,
+                                   d.stride_w, 0, 0, d.groups, &bordered) == CNN_OK &&
+                        bordered.P == p.conv.P && bordered.Q == p.conv.Q) {
+                        p.conv = bordered;
+                        plan[prev_exec].opad_h = d.pad_h;
+                        plan[prev_exec].opad_w = d.pad_w;
+                        mx = std::max<int64_t>(mx, (int64_t)N * c * hb * wb);
+                    }
+                }
                 c = d.out_channels; h = p.conv.P; w = p.conv.Q;
                 p.relu = d.fuse_relu != 0;
                 if (N > 0) {
@@ -382,7 +403,8 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
                 if (p.lrn_from >= 0) {  // cur is still the LRN's input
                     const cnn_layer_desc& ld = L[p.lrn_from];
                     rc = launch_lrn_pool(p.pool, d.pool_mode, p.relu, ld.lrn_size, ld.lrn_alpha,
-                                         ld.lrn_beta, ld.lrn_k, cur, out, d.pool_index, st, relu_in, fj);
+                                         ld.lrn_beta, ld.lrn_k, cur, out, d.pool_index, st, relu_in, fj,
+                                         p.opad_h, p.opad_w);
                 } else {
                     rc = launch_pool(p.pool, d.pool_mode, p.relu, cur, out, d.pool_index, st, relu_in, fj);
                 }

@@ -275,10 +275,11 @@ struct LrnPoolParams {
     int CB, PB, RB;   // channels, output rows and input rows per workgroup
     int nchunk, nband;
     int relu_x;       // take the input through a ReLU as it is read
-    FastDiv f_plane, f_w, f_pbq, f_q;  // RB*W, W, PB*Q, Q
+    FastDiv f_plane, f_w, f_pbq, f_q;  // RB*W, W, PB*OQ, OQ (OQ = Q + 2 opad_w)
     int relu;
     float alpha_over_size, beta, k;
-    FillJobs fills;  // bias fills run after the pooling (n = 0: none)
+    int opad_h, opad_w;  // y holds each plane inside a zero border of this width
+    FillJobs fills;      // bias fills run after the pooling (n = 0: none)
 };
 
 template <int HALF, int CC, int MODE, bool WITH_IDX>  // MODE 0: max, 1: average
@@ -333,44 +334,64 @@ __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
     }
     __syncthreads();
 
-    // 3. pooling from the LRN tile
+    // 3. pooling from the LRN tile.  Work-item (c, pr, qq) is column qq of
+    //    y's row for output row p0 + pr, border columns included, so that
+    //    every row of y is written whole (border columns get 0).
     const int PQ = p.P * p.Q;
-    const int pbq = p.PB * p.Q;
+    const int OQ = p.Q + 2 * p.opad_w, OPQ = (p.P + 2 * p.opad_h) * OQ;  // y's plane
+    const int pbq = p.PB * OQ;
     const int nout = p.CB * pbq;
     for (int o = threadIdx.x; o < nout; o += kThreads) {
         const int c = (int)fdiv(o, p.f_pbq);
         const int rq = o - c * pbq;
         const int pr = (int)fdiv(rq, p.f_q);
-        const int q = rq - pr * p.Q;
+        const int qq = rq - pr * OQ;
         const int pp = p0 + pr;
         if (c0 + c >= p.C || pp >= pend) continue;
-        const int hs = pp * p.sh - p.ph, ws = q * p.sw - p.pw;
-        const int h0 = max(hs, 0), w0 = max(ws, 0);
-        const int h1 = min(hs + p.kh, p.H), w1 = min(ws + p.kw, p.W);
-        const float* t = lrn + c * plane;
-        float out;
-        if constexpr (MODE == 0) {
-            int bi = h0 * p.W + w0;  // first maximum in row-major order
-            float best = t[(h0 - row0) * p.W + w0];
-            for (int h = h0; h < h1; ++h)
-                for (int w = w0; w < w1; ++w) {
-                    const float v = t[(h - row0) * p.W + w];
-                    if (v > best) {
-                        best = v;
-                        bi = h * p.W + w;
+        const int q = qq - p.opad_w;
+        float out = 0.0f;
+        if ((unsigned)q < (unsigned)p.Q) {
+            const int hs = pp * p.sh - p.ph, ws = q * p.sw - p.pw;
+            const int h0 = max(hs, 0), w0 = max(ws, 0);
+            const int h1 = min(hs + p.kh, p.H), w1 = min(ws + p.kw, p.W);
+            const float* t = lrn + c * plane;
+            if constexpr (MODE == 0) {
+                int bi = h0 * p.W + w0;  // first maximum in row-major order
+                float best = t[(h0 - row0) * p.W + w0];
+                for (int h = h0; h < h1; ++h)
+                    for (int w = w0; w < w1; ++w) {
+                        const float v = t[(h - row0) * p.W + w];
+                        if (v > best) {
+                            best = v;
+                            bi = h * p.W + w;
+                        }
                     }
-                }
-            out = best;
-            if (WITH_IDX) p.idx[(size_t)(n * p.C + c0 + c) * PQ + pp * p.Q + q] = bi;
-        } else {
-            const int count = (min(hs + p.kh, p.H + p.ph) - hs) * (min(ws + p.kw, p.W + p.pw) - ws);
-            float sum = 0.0f;
-            for (int h = h0; h < h1; ++h)
-                for (int w = w0; w < w1; ++w) sum += t[(h - row0) * p.W + w];
-            out = sum / (float)count;
+                out = best;
+                if (WITH_IDX) p.idx[(size_t)(n * p.C + c0 + c) * PQ + pp * p.Q + q] = bi;
+            } else {
+                const int count = (min(hs + p.kh, p.H + p.ph) - hs) * (min(ws + p.kw, p.W + p.pw) - ws);
+                float sum = 0.0f;
+                for (int h = h0; h < h1; ++h)
+                    for (int w = w0; w < w1; ++w) sum += t[(h - row0) * p.W + w];
+                out = sum / (float)count;
+            }
+            if (p.relu) out = out > 0.0f ? out : 0.0f;
         }
-        if (p.relu) out = out > 0.0f ? out : 0.0f;
-        p.y[(size_t)(n * p.C + c0 + c) * PQ + pp * p.Q + q] = out;
+        p.y[(size_t)(n * p.C + c0 + c) * OPQ + (pp + p.opad_h) * OQ + qq] = out;
+    }
+
+    // 4. y's border rows above the first band and below the last, whole rows
+    if (p.opad_h > 0 && (p0 == 0 || pend == p.P)) {
+        const int per_c = p.opad_h * OQ;  // border elements above (or below) a plane
+        const int nedge = (p0 == 0) + (pend == p.P);
+        for (int o = threadIdx.x; o < p.CB * nedge * per_c; o += kThreads) {
+            const int ce = o / per_c;  // (channel, edge)
+            const int e = o - ce * per_c;
+            const int c = ce / nedge;
+            const bool below = (ce - c * nedge) == 1 || p0 != 0;
+            const int off = below ? (p.opad_h + p.P) * OQ + e : e;
+            if (c0 + c < p.C) p.y[(size_t)(n * p.C + c0 + c) * OPQ + off] = 0.0f;
+        }
     }
     run_fills(p.fills);
 }
@@ -574,7 +595,7 @@ bool lrn_pool_fusable(const PoolShape& s, int size) {
 
 int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alpha, float beta, float k,
                     const float* x, float* y, int32_t* idx, hipStream_t st, bool relu_x,
-                    const FillJobs* fills) {
+                    const FillJobs* fills, int opad_h, int opad_w) {
     if (s.N == 0) return fills ? launch_bias_fills(fills->job, fills->n, st) : CNN_OK;
     const int half = size / 2;
     LrnPoolTiling t;
@@ -593,13 +614,15 @@ int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alph
     p.nband = ceil_div(s.P, p.PB);
     p.f_plane = make_fastdiv(p.RB * s.W);
     p.f_w = make_fastdiv(s.W);
-    p.f_pbq = make_fastdiv(p.PB * s.Q);
-    p.f_q = make_fastdiv(s.Q);
+    p.f_pbq = make_fastdiv(p.PB * (s.Q + 2 * opad_w));  // y's rows hold the border columns too
+    p.f_q = make_fastdiv(s.Q + 2 * opad_w);
     p.relu = relu;
     p.alpha_over_size = alpha / (float)size;
     p.beta = beta;
     p.k = k;
     p.relu_x = relu_x;
+    p.opad_h = opad_h;
+    p.opad_w = opad_w;
     p.fills.n = 0;
     if (fills) p.fills = *fills;
     const size_t shm = (size_t)p.CB * p.RB * s.W * 4;

@@ -103,11 +103,14 @@ int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha
 int launch_relu(const float* x, float* y, int64_t n, hipStream_t st);
 // LRN (across channels, odd size) followed by pooling of its output, in one
 // kernel; s is the pooling shape (its input is the LRN's shape).  Only where
-// lrn_pool_fusable() holds.
+// lrn_pool_fusable() holds.  opad_h, opad_w > 0: y holds each output plane
+// inside a zero border of that width ((P + 2 opad_h) x (Q + 2 opad_w) per
+// plane), the input layout of a padded convolution run as unpadded; idx keeps
+// the plain P x Q layout.
 bool lrn_pool_fusable(const PoolShape& s, int size);
 int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alpha, float beta, float k,
                     const float* x, float* y, int32_t* idx, hipStream_t st, bool relu_x = false,
-                    const FillJobs* fills = nullptr);
+                    const FillJobs* fills = nullptr, int opad_h = 0, int opad_w = 0);
 int launch_softmax(const float* x, int N, int C, int HW, float* y, hipStream_t st);
 
 }  // namespace cnn
