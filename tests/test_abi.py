@@ -248,3 +248,23 @@ def test_tuning_table_text_roundtrip():
         == cnn.CNN_ERR_INVALID
     cnn.cnn_tuning_clear()
     assert cnn.cnn_tuning_export() == ""
+
+
+def test_workspace_holds_bordered_pool_output():
+    """A padded conv after LRN + pooling reads the pooled planes inside their
+    zero border: the workspace holds two buffers of the bordered size when
+    that is the largest activation (8 x 34 x 34 here, against 8 x 30 x 30 for
+    the LRN and the 3x3/1 pooling and 4 x 30 x 30 out of the conv, the last
+    layer)."""
+    net = wl.Net("lrn_pool_conv", (8, 30, 30), (
+        wl.lrn(5, 1e-4, 0.75, 1.0), wl.pool("max", 3, 1, 1), wl.conv(8, 4, 5, 1, 2)), 0.1, 0.1)
+    descs = _descs(net)
+    for N in (1, 7, 64):
+        ws = cnn.lib.cnn_net_workspace_bytes(descs, len(descs), N, 8, 30, 30)
+        half = (N * 8 * 34 * 34 * 4 + 255) // 256 * 256
+        assert ws == 2 * half, (N, ws, half)
+    # without the LRN the pooling kernel writes plain planes (and the conv pads)
+    plain = wl.Net("pool_conv", (8, 30, 30), (wl.pool("max", 3, 1, 1), wl.conv(8, 4, 5, 1, 2)), 0.1, 0.1)
+    descs = _descs(plain)
+    ws = cnn.lib.cnn_net_workspace_bytes(descs, len(descs), 7, 8, 30, 30)
+    assert ws == 2 * ((7 * 8 * 30 * 30 * 4 + 255) // 256 * 256)

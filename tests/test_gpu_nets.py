@@ -270,24 +270,27 @@ def test_replicas_run_concurrently_on_two_streams(gpu):
 
 @pytest.mark.parametrize("batch", [1, 3, 16])
 @pytest.mark.parametrize("pad", [(1, 1), (2, 1), (2, 2)])
-def test_padded_conv_after_lrn_pool(gpu, batch, pad):
+@pytest.mark.parametrize("pool", [("max", 3, 2, 0), ("avg", 3, 1, 1)])
+def test_padded_conv_after_lrn_pool(gpu, batch, pad, pool):
     """An LRN + pooling kernel followed by a padded convolution writes its
     output planes inside a zero border and the convolution runs unpadded on
     them.  Several bands and channel chunks per image, border widths that
     differ by axis, a ReLU folded into the pooling, and max-pool indices,
     which keep the plain layout."""
-    print(f"lrn+pool -> conv pad {pad} batch {batch}", flush=True)
+    mode, pk, ps, pp = pool
+    print(f"lrn+pool {pool} -> conv pad {pad} batch {batch}", flush=True)
     k = (2 * pad[0] + 1, 2 * pad[1] + 1)
+    P, Q = oracle.pool_out_shape(29, 23, pk, pk, ps, ps, pp, pp)
     net = wl.Net("lrn_pool_conv", (40, 29, 23), (
-        wl.lrn(5, 1e-2, 0.75, 2.0), wl.pool("max", 3, 2), wl.relu(),
+        wl.lrn(5, 1e-2, 0.75, 2.0), wl.pool(mode, pk, ps, pp), wl.relu(),
         wl.conv(40, 24, k, 1, pad, 2, relu=True),
-        wl.fc(24 * 14 * 11, 10),
+        wl.fc(24 * P * Q, 10),
     ), 0.1, 0.1, input_dist="normal")
     x = wl.make_input(net, batch, 16) * 3
     params = wl.make_params(net, 16)
-    model = gpu.Network(net, params, pool_index=True)
+    model = gpu.Network(net, params, pool_index=(mode == "max"))
     outs = oracle.net_fwd(net, x, params, keep=True, pool_index=True)
     y = to_host(model(to_dev(x)))
-    assert_gemm_close(y, outs[0], 24 * 14 * 11, f"pad {pad} B{batch}")
-    ref_idx = outs[2][1]
-    assert np.mean(to_host(model.indices[1]) == ref_idx) > 0.999
+    assert_gemm_close(y, outs[0], 24 * P * Q, f"{pool} pad {pad} B{batch}")
+    if mode == "max":
+        assert np.mean(to_host(model.indices[1]) == outs[2][1]) > 0.999
