@@ -410,3 +410,36 @@ def test_softmax_in_place_large_values_and_empty(gpu):
     gpu.cnn_softmax_fwd(xd, y=xd)
     np.testing.assert_allclose(to_host(xd), oracle.softmax_fwd(x4), rtol=_softmax_rtol(x4, 9), atol=1e-37)
     assert gpu.cnn_softmax_fwd(torch.empty((0, 10), device="cuda")).shape == (0, 10)
+
+
+# ---------------------------------------------------------------- random shapes
+def _random_conv(seed):
+    """A seeded random convolution: rectangular filters up to 7x7, strides
+    and paddings per axis, groups, a tile configuration drawn from all of
+    them (or the heuristic), batches that split or not."""
+    rng = np.random.default_rng(9000 + seed)
+    G = int(rng.choice([1, 1, 1, 2, 3, 4]))
+    C = G * int(rng.integers(1, 17))
+    K = G * int(rng.integers(1, 49))
+    R, S = (int(v) for v in rng.integers(1, 8, size=2))
+    sh, sw = (int(v) for v in rng.integers(1, 4, size=2))
+    ph, pw = int(rng.integers(0, R)), int(rng.integers(0, S))
+    H = int(rng.integers(max(1, R - 2 * ph), 33))
+    W = int(rng.integers(max(1, S - 2 * pw), 33))
+    N = int(rng.choice([1, 2, 3, 5, 9]))
+    return N, C, H, W, K, R, S, (sh, sw), (ph, pw), G
+
+
+@pytest.mark.parametrize("seed", range(48))
+def test_conv_random_shapes(gpu, seed):
+    N, C, H, W, K, R, S, st, pd, G = _random_conv(seed)
+    cfg = int(np.random.default_rng(seed).integers(-1, gpu.cnn_conv2d_num_configs()))
+    tag = f"random conv {seed}: N{N} C{C} {H}x{W} K{K} {R}x{S} s{st} p{pd} G{G} cfg{cfg}"
+    print(tag, flush=True)
+    x = wl.normal((N, C, H, W), 1.0, 40 + seed, 0)
+    w = wl.normal((K, C // G, R, S), 1.0, 40 + seed, 1)
+    b = wl.normal((K,), 1.0, 40 + seed, 2)
+    y = gpu.cnn_conv2d_fwd(to_dev(x), to_dev(w), to_dev(b), st, pd, G, True, config=cfg)
+    ref = oracle.conv2d_fwd(x, w, b, st, pd, G, True)
+    assert_gemm_close(to_host(y), ref, (C // G) * R * S, tag)
+
