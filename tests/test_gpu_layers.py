@@ -443,3 +443,72 @@ def test_conv_random_shapes(gpu, seed):
     ref = oracle.conv2d_fwd(x, w, b, st, pd, G, True)
     assert_gemm_close(to_host(y), ref, (C // G) * R * S, tag)
 
+
+
+def _random_pool(seed):
+    """Seeded random pooling: windows up to 5x5 per axis, strides, paddings
+    below the window, ceil or floor, planes small enough to stage in LDS and
+    (one case in four) too large for it."""
+    rng = np.random.default_rng(9500 + seed)
+    kh, kw = (int(v) for v in rng.integers(1, 6, size=2))
+    sh, sw = (int(v) for v in rng.integers(1, 5, size=2))
+    ph, pw = int(rng.integers(0, kh)), int(rng.integers(0, kw))
+    big = seed % 4 == 3
+    H = int(rng.integers(max(1, kh - 2 * ph), 90 if big else 40))
+    W = int(rng.integers(max(1, kw - 2 * pw), 90 if big else 40))
+    if big:
+        H, W = max(H, 66), max(W, 66)  # planes above 16 KiB
+    N, C = int(rng.integers(1, 4)), int(rng.integers(1, 20))
+    mode = "max" if seed % 2 == 0 else "avg"
+    return N, C, H, W, mode, (kh, kw), (sh, sw), (ph, pw), bool(rng.integers(0, 2)), bool(seed % 3 == 1)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_pool_random_shapes(gpu, seed):
+    N, C, H, W, mode, k, s, p, ceil, relu = _random_pool(seed)
+    tag = f"random pool {seed}: N{N} C{C} {H}x{W} {mode} k{k} s{s} p{p} ceil{int(ceil)} relu{int(relu)}"
+    print(tag, flush=True)
+    x = wl.normal((N, C, H, W), 1.0, 60 + seed, 0)
+    if mode == "max":
+        yg, ig = gpu.cnn_pool_fwd(to_dev(x), "max", k, s, p, ceil, relu, with_index=True)
+        yr, ir = oracle.pool_fwd(x, "max", k, s, p, ceil, relu, with_index=True)
+        np.testing.assert_array_equal(to_host(yg), yr, err_msg=tag)
+        np.testing.assert_array_equal(to_host(ig), ir, err_msg=tag)
+    else:
+        yg = gpu.cnn_pool_fwd(to_dev(x), "avg", k, s, p, ceil, relu)
+        yr = oracle.pool_fwd(x, "avg", k, s, p, ceil, relu)
+        assert_elementwise_close(to_host(yg), yr, np.abs(x).max(), tag)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_fc_random_shapes(gpu, seed):
+    """Seeded random FC layers: batches from 1 (matrix-vector kernel) to 70,
+    reductions that are and are not multiples of 4, with and without bias
+    and ReLU."""
+    rng = np.random.default_rng(9700 + seed)
+    N = int(rng.choice([1, 2, 3, 7, 16, 31, 33, 64, 70]))
+    I, O = int(rng.integers(1, 3000)), int(rng.integers(1, 700))
+    relu, bias = bool(rng.integers(0, 2)), bool(rng.integers(0, 4))
+    tag = f"random fc {seed}: N{N} I{I} O{O} relu{int(relu)} bias{int(bias)}"
+    print(tag, flush=True)
+    x = wl.normal((N, I), 1.0, 80 + seed, 0)
+    w = wl.normal((O, I), 1.0, 80 + seed, 1)
+    b = wl.normal((O,), 1.0, 80 + seed, 2) if bias else None
+    yg = gpu.cnn_fc_fwd(to_dev(x), to_dev(w), to_dev(b) if bias else None, relu)
+    assert_gemm_close(to_host(yg), oracle.fc_fwd(x, w, b, relu), I, tag)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_lrn_random_shapes(gpu, seed):
+    """Seeded random LRN: every odd size to 11 (the wide-window kernel above
+    9), channel counts on both sides of the 32-channel chunk."""
+    rng = np.random.default_rng(9900 + seed)
+    size = int(rng.choice([1, 3, 5, 7, 9, 11]))
+    N, C = int(rng.integers(1, 4)), int(rng.integers(1, 80))
+    H, W = (int(v) for v in rng.integers(1, 30, size=2))
+    alpha, beta, k = float(rng.uniform(1e-4, 0.1)), float(rng.uniform(0.5, 0.9)), float(rng.uniform(1.0, 2.0))
+    tag = f"random lrn {seed}: N{N} C{C} {H}x{W} size{size} a{alpha:.4f} b{beta:.3f} k{k:.3f}"
+    print(tag, flush=True)
+    x = wl.normal((N, C, H, W), 3.0, 90 + seed, 0)
+    yg = to_host(gpu.cnn_lrn_fwd(to_dev(x), size, alpha, beta, k))
+    assert_elementwise_close(yg, oracle.lrn_fwd(x, size, alpha, beta, k), np.abs(x).max(), tag)
