@@ -209,7 +209,10 @@ int cnn_net_out_shape(const cnn_layer_desc* layers, int n_layers, int N, int C,
                       int H, int W, int* outC, int* outH, int* outW);
 
 /* Device workspace cnn_net_fwd needs for this input: two activation buffers
- * of the largest intermediate tensor, each 256-byte aligned, plus room for
+ * of the largest intermediate tensor, each 256-byte aligned (a pooling layer
+ * run with its LRN writes its planes inside the zero border of a padded CONV
+ * layer that reads them, which then runs unpadded: such planes count with
+ * their border), plus room for
  * the outputs of the conv and FC layers whose reduction may be split across
  * workgroups (small outputs, e.g. at batch 1; they are set to their biases
  * together, by the pooling kernel that runs just before the first of them,
