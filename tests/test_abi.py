@@ -268,3 +268,18 @@ def test_workspace_holds_bordered_pool_output():
     descs = _descs(plain)
     ws = cnn.lib.cnn_net_workspace_bytes(descs, len(descs), 7, 8, 30, 30)
     assert ws == 2 * ((7 * 8 * 30 * 30 * 4 + 255) // 256 * 256)
+
+
+def test_binding_refuses_to_load_without_the_library(tmp_path):
+    """A copy of the package without libcnn.so raises on import: there is no
+    fallback path that could compute anything without the HIP library."""
+    import shutil
+    import subprocess
+    import sys
+    pkg = os.path.join(ROOT, "paper_1511_07376_amd")
+    dst = tmp_path / "paper_1511_07376_amd"
+    shutil.copytree(pkg, dst, ignore=shutil.ignore_patterns("libcnn.so", "_build", "__pycache__", "csrc"))
+    code = "import paper_1511_07376_amd.cnn"
+    r = subprocess.run([sys.executable, "-c", code], cwd=tmp_path, capture_output=True, text=True, timeout=120)
+    assert r.returncode != 0
+    assert "libcnn.so is missing" in r.stderr
