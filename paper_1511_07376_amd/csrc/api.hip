@@ -201,8 +201,9 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
                 if ((d.pad_h > 0 || d.pad_w > 0) && prev_exec >= 0 && plan[prev_exec].type == CNN_LAYER_POOL &&
                     plan[prev_exec].lrn_from >= 0) {
                     ConvShape bordered;
-                    const int hb = h + 2 * d.pad_h, wb = w + 2 * d.pad_w;
-                    if (hb > h && wb > w &&
+                    const int64_t hb64 = (int64_t)h + 2 * (int64_t)d.pad_h, wb64 = (int64_t)w + 2 * (int64_t)d.pad_w;
+                    const int hb = (int)std::min<int64_t>(hb64, INT32_MAX), wb = (int)std::min<int64_t>(wb64, INT32_MAX);
+                    if (hb64 <= INT32_MAX && wb64 <= INT32_MAX &&
                         check_conv(N, c, hb, wb, d.out_channels, d.kernel_h, d.kernel_w, d.stride_h,
                                    d.stride_w, 0, 0, d.groups, &bordered) == CNN_OK &&
                         bordered.P == p.conv.P && bordered.Q == p.conv.Q) {

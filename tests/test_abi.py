@@ -283,3 +283,15 @@ def test_binding_refuses_to_load_without_the_library(tmp_path):
     r = subprocess.run([sys.executable, "-c", code], cwd=tmp_path, capture_output=True, text=True, timeout=120)
     assert r.returncode != 0
     assert "libcnn.so is missing" in r.stderr
+
+
+def test_bordered_planning_with_extreme_padding():
+    """The bordered input extent (pooled plane + 2 x pad) is formed in 64
+    bits: with a padding near 2^30 (and a stride that keeps the conv output
+    small) the planner falls back to the padded conv instead of wrapping."""
+    net = wl.Net("x", (8, 30, 30), (wl.lrn(5, 1e-4, 0.75, 1.0), wl.pool("max", 3, 2),
+                                     wl.conv(8, 4, 3, 2**30, 2**30)), 0.1, 0.1)
+    descs = _descs(net)
+    assert cnn.cnn_conv2d_out_shape(15, 15, 3, 3, 2**30, 2**30) == (3, 3)
+    ws = cnn.lib.cnn_net_workspace_bytes(descs, len(descs), 2, 8, 30, 30)
+    assert ws == 2 * ((2 * 8 * 30 * 30 * 4 + 255) // 256 * 256)  # the LRN's output is the largest
