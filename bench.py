@@ -456,7 +456,7 @@ def main():
         "ms_per_step_with_layer_events": round(ms_step_events, 4),
         "ms_per_step_with_layer_events_median": round(float(np.median(step_ms_events)), 4),
         "graph_replay": bool(graph is not None),
-        "streams": args.streams,
+        "streams": args.streams if graph is None else 1,
         "autotune": bool(args.autotune),
         "conv_configs": {" ".join(l.split()[:-1]): cnn.cnn_conv2d_config_name(int(l.split()[-1]))
                          for l in cnn.cnn_tuning_export().splitlines()},
