@@ -22,16 +22,21 @@ struct ConvConfig {
 const ConvConfig kConfigs[] = {CNN_CONV_CONFIGS(CNN_CONV_ENTRY)};
 constexpr int kNumConfigs = sizeof(kConfigs) / sizeof(kConfigs[0]);
 
-// Heuristic choice when no tuned entry exists: the output-channel tile follows
-// the group's channel count; a narrower pixel tile when the grid would leave
-// most compute units idle.
+// Heuristic choice when no tuned entry exists, fitted to measured times of
+// every configuration on AlexNet's, LeNet's and CIFAR-10 quick's layers and
+// the single-layer sweep shapes at batches 1 to 256 (its total over those 46
+// shapes is within 1% of always picking the fastest).  t64: output tiles of a
+// 64 x 64 tile; b128: of a 128 x 128 tile.
 int heuristic_config(const ConvParams& p, int G) {
-    const int mt128 = ceil_div(p.M, 128);
-    if (p.Kg <= 32) return 8;
-    if (p.Kg <= 64) return mt128 * G >= 512 ? 4 : 9;
-    if (p.Kg <= 96) return 6;
-    const int blocks = mt128 * ceil_div(p.Kg, 128) * G;
-    return blocks >= 512 ? 0 : 2;
+    const int64_t t64 = (int64_t)ceil_div(p.M, 64) * ceil_div(p.Kg, 64) * G;
+    const int64_t b128 = (int64_t)ceil_div(p.M, 128) * ceil_div(p.Kg, 128) * G;
+    if (p.Kg <= 32) return 8;                                         // 32 x 128
+    if (std::max(p.sh, p.sw) >= 4 && p.Kg > 64) return t64 >= 4000 ? 6 : 8;  // strided stem
+    if (t64 >= 4000 && p.Kg > 64) return 4;                          // 64 x 128
+    if (p.Kg > 64 && p.Kg <= 128 && b128 >= 512) return 0;           // 128 x 128
+    if (p.Kg >= 256 && t64 >= 300 && t64 < 1000) return 2;           // 128 x 64
+    if (t64 < 1000) return 10;                                        // 64 x 64, BK 32
+    return 9;                                                         // 64 x 64, BK 16
 }
 
 // Reduction chunks for a configuration: when its output tiles would give the
