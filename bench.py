@@ -106,36 +106,70 @@ def stored_traffic(workload, layer_name):
     return None if lay is None else lay.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(net, x, params, budget_s):
+def host_cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(net, x, params, budget_s, y_gpu=None):
+    """Times the oracle on a bounded sample of the batch, and checks the GPU
+    output of every image the oracle computed against it (the conv / FC
+    criterion of the last layer).  Returns (record, parity record)."""
     import oracle
     threads = oracle.get_threads()
     t0 = time.perf_counter()
-    oracle.net_fwd(net, x[:1], params)
+    ref0 = oracle.net_fwd(net, x[:1], params)
     t1 = time.perf_counter() - t0
     n_more = int(max(0, min(x.shape[0] - 1, (budget_s - t1) / max(t1, 1e-3))))
     t2 = 0.0
     reps = 0
     n = 1
+    refs = [ref0]
     if n_more > 0:
         # the same images again while less than ~2/3 of the budget is spent,
         # so that a fast oracle pass is still timed over several seconds
         while reps == 0 or (t1 + t2 < 0.67 * budget_s and reps < 10000):
             t0 = time.perf_counter()
-            oracle.net_fwd(net, x[1:1 + n_more], params)
+            r = oracle.net_fwd(net, x[1:1 + n_more], params)
             t2 += time.perf_counter() - t0
+            if reps == 0:
+                refs.append(r)
             reps += 1
         n = 1 + reps * n_more
-    # the paper's sequential baseline: one thread, one image
+    # the paper's sequential baseline: one thread, one image, mean of 3 runs
     oracle.set_threads(1)
-    t0 = time.perf_counter()
-    oracle.net_fwd(net, x[:1], params)
-    t_one = time.perf_counter() - t0
+    t_one = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        oracle.net_fwd(net, x[:1], params)
+        t_one.append(time.perf_counter() - t0)
     oracle.set_threads(threads)
-    return {"value": n / (t1 + t2), "unit": "images/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n} images ({max(reps, 1)} pass(es) over {1 + n_more} of the {x.shape[0]} images of "
-                      f"the same batch) through the oracle's layer-by-layer network (double "
-                      f"accumulation, OpenMP over images x channels), {t1 + t2:.1f} s",
-            "value_1_thread": round(1.0 / t_one, 3)}
+    rec = {"value": n / (t1 + t2), "unit": "images/s", "cores": threads, "kind": "oracle",
+           "sample": f"{n} images ({max(reps, 1)} pass(es) over {1 + n_more} of the {x.shape[0]} images of "
+                     f"the same batch) through the oracle's layer-by-layer network (double "
+                     f"accumulation, OpenMP over images x channels), {t1 + t2:.1f} s",
+           "host_cpu": host_cpu_model(), "host_threads_available": os.cpu_count(),
+           "value_1_thread": round(1.0 / float(np.mean(t_one)), 3),
+           "value_1_thread_runs_s": [round(t, 3) for t in t_one]}
+    parity = None
+    if y_gpu is not None:
+        ref = np.concatenate(refs, axis=0).astype(np.float64)
+        got = y_gpu[: ref.shape[0]].reshape(ref.shape).astype(np.float64)
+        last = [l for l in net.layers if l.kind in ("conv", "fc")][-1]
+        kred = last.in_features if last.kind == "fc" else \
+            (last.in_channels // last.groups) * last.kernel[0] * last.kernel[1]
+        err = float(np.abs(got - ref).max())
+        rel = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300))
+        tol = 1e-4 * np.sqrt(kred)
+        parity = {"images_checked": int(ref.shape[0]), "max_abs_err": err, "abs_tol": float(tol),
+                  "rel_l2_err": rel, "rel_tol": 1e-4, "ok": bool(err <= tol and rel <= 1e-4)}
+    return rec, parity
 
 
 def conv_sweep(args):
@@ -464,12 +498,18 @@ def main():
         "roofline": roof,
     }
     if args.cpu_budget > 0:
-        cb = cpu_baseline(net, x, params, args.cpu_budget)
+        cb, parity = cpu_baseline(net, x, params, args.cpu_budget, yd.cpu().numpy())
         result["cpu_baseline"] = cb
+        # the timed pass's output, checked against the oracle on every image
+        # the baseline computed
+        result["parity_vs_oracle"] = parity
         # the paper's speedups are GPU vs the sequential CPU implementation
         result["speedup_vs_oracle"] = {"all_cores": round(result["value"] / cb["value"], 1),
                                        "one_thread": round(result["value"] / cb["value_1_thread"], 1)}
     print(json.dumps(result), flush=True)
+    if result.get("parity_vs_oracle") and not result["parity_vs_oracle"]["ok"]:
+        print(f"bench: the timed output differs from the oracle: {result['parity_vs_oracle']}", file=sys.stderr)
+        sys.exit(1)
 
 
 if __name__ == "__main__":

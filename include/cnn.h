@@ -245,6 +245,32 @@ int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x
                       int N, int C, int H, int W, float* y, void* ws,
                       size_t ws_bytes, void* const* events, cnn_stream_t stream);
 
+/* As cnn_net_fwd, and also writes every layer's output, so that each layer of
+ * a network pass can be compared with a reference of that layer (the paper
+ * checks only the last layer's output, Sec. 4.1).  A checking aid: the copies
+ * cost time and the call is not meant for timing.
+ *   dumps    host array of n_layers DEVICE pointers (the array itself must not
+ *            be NULL).  dumps[i] NULL: nothing is written for layer i;
+ *            otherwise a caller-owned buffer of N*outC*outH*outW floats (the
+ *            shape of cnn_net_out_shape over the first i+1 layers) that
+ *            receives layer i's output as the layer list defines it: plain
+ *            NCHW without the zero border a pooling layer may give its planes
+ *            for the padded conv after it, and after the layer's own ReLU even
+ *            where the kernel left that ReLU to the next layer's reads.  An
+ *            LRN layer run inside the pooling layer after it is run once more
+ *            on its own (bit-identical to the fused kernel's LRN values) to
+ *            fill its dump.
+ *   written  host array of n_layers ints, or NULL: written[i] = 1 where
+ *            dumps[i] was filled, 0 where it was NULL or where layer i is a
+ *            RELU layer executed inside its predecessor (that predecessor's
+ *            dump then holds the output after this ReLU).
+ * Validation, errors and the workspace are those of cnn_net_fwd; a dump
+ * buffer must not overlap x, y, ws or another dump. */
+int cnn_net_fwd_dump(const cnn_layer_desc* layers, int n_layers, const float* x,
+                     int N, int C, int H, int W, float* y, void* ws,
+                     size_t ws_bytes, float* const* dumps, int* written,
+                     cnn_stream_t stream);
+
 /* ---------------------------------------------------------------- execution
  * The paper's engine runs a network either sequentially or in parallel, as
  * the NetFile's execution_mode says (Sec. 3.5).  Here every layer runs on the

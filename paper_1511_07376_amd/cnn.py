@@ -77,6 +77,8 @@ lib.cnn_net_workspace_bytes.restype = ctypes.c_size_t
 lib.cnn_net_fwd.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t, _p]
 lib.cnn_net_fwd_timed.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
                                   ctypes.POINTER(ctypes.c_void_p), _p]
+lib.cnn_net_fwd_dump.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
+                                 ctypes.POINTER(ctypes.c_void_p), _ip, _p]
 lib.cnn_conv2d_fwd_config.argtypes = lib.cnn_conv2d_fwd.argtypes[:17] + [_i, _p]
 lib.cnn_netfile_parse.argtypes = [ctypes.c_char_p, _descp, _i, _ip, ctypes.POINTER(cnn_netfile_config)]
 lib.cnn_net_graph_create.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
@@ -96,14 +98,15 @@ lib.cnn_version.restype = ctypes.c_char_p
 for _name in ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
               "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_softmax_fwd", "cnn_net_out_shape",
               "cnn_net_fwd",
-              "cnn_net_fwd_timed", "cnn_conv2d_fwd_config", "cnn_conv2d_num_configs",
+              "cnn_net_fwd_timed", "cnn_net_fwd_dump", "cnn_conv2d_fwd_config", "cnn_conv2d_num_configs",
               "cnn_set_autotune", "cnn_tuning_import", "cnn_tuning_clear", "cnn_netfile_parse",
               "cnn_net_graph_create", "cnn_net_graph_launch", "cnn_net_graph_destroy"):
     getattr(lib, _name).restype = _i
 
 EXPORTED = ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
             "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_softmax_fwd", "cnn_net_out_shape",
-            "cnn_net_workspace_bytes", "cnn_net_fwd", "cnn_net_fwd_timed", "cnn_last_error",
+            "cnn_net_workspace_bytes", "cnn_net_fwd", "cnn_net_fwd_timed", "cnn_net_fwd_dump",
+            "cnn_last_error",
             "cnn_version", "cnn_conv2d_num_configs", "cnn_conv2d_config_name",
             "cnn_conv2d_fwd_config", "cnn_set_autotune", "cnn_tuning_export",
             "cnn_tuning_import", "cnn_tuning_clear", "cnn_netfile_parse", "cnn_net_graph_create",
@@ -548,6 +551,38 @@ class Network:
         return y
 
     __call__ = forward
+
+    def layer_shapes(self, N: int) -> List[Tuple[int, ...]]:
+        """Output shape of every layer for a batch of N (the library's shape rules)."""
+        C, H, W = self.net.input_chw
+        oc, oh, ow = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+        shapes = []
+        flat = False  # after an FC layer (and the ReLU / softmax layers after it): [N][O]
+        for i, layer in enumerate(self.net.layers):
+            _ok(lib.cnn_net_out_shape(self.descs, i + 1, N, C, H, W, ctypes.byref(oc),
+                                      ctypes.byref(oh), ctypes.byref(ow)))
+            if layer.kind not in ("relu", "softmax"):
+                flat = layer.kind == "fc"
+            shapes.append((N, oc.value) if flat else (N, oc.value, oh.value, ow.value))
+        return shapes
+
+    def forward_dump(self, x: torch.Tensor, y: Optional[torch.Tensor] = None, stream=None):
+        """cnn_net_fwd_dump: one pass that also writes every layer's output.
+
+        Returns (y, outs, written): outs[i] is layer i's output (a tensor of
+        its shape) where written[i], else None (a RELU layer executed inside
+        its predecessor, whose entry then holds the output after it)."""
+        N, C, H, W = x.shape
+        self._prepare(N)
+        if y is None:
+            y = torch.empty(self.out_shape(N), dtype=torch.float32, device=x.device)
+        bufs = [torch.empty(s, dtype=torch.float32, device=x.device) for s in self.layer_shapes(N)]
+        ptrs = (ctypes.c_void_p * len(bufs))(*[b.data_ptr() for b in bufs])
+        written = (ctypes.c_int * len(bufs))()
+        _ok(lib.cnn_net_fwd_dump(self.descs, len(self.descs), _dev(x, "x"), N, C, H, W, _dev(y, "y"),
+                                 self._ws.data_ptr(), self._ws.numel(), ptrs, written, _stream(stream)))
+        flags = [bool(written[i]) for i in range(len(bufs))]
+        return y, [b if f else None for b, f in zip(bufs, flags)], flags
 
 
 def cnn_net_fwd(network: Network, x, y=None, stream=None):

@@ -300,8 +300,14 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
     return CNN_OK;
 }
 
+// dumps (may be null): per layer, a device buffer that receives the layer's
+// output as the layer list defines it (written[i] = 1), or nothing (written[i]
+// = 0) for a RELU layer executed inside its predecessor, whose dump then holds
+// the output after that ReLU.  An LRN run inside the pooling layer after it is
+// also run on its own into its dump (the fused kernel never stores it).
 int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H, int W, float* y,
-            void* ws, size_t ws_bytes, void* const* events, hipStream_t st) {
+            void* ws, size_t ws_bytes, void* const* events, hipStream_t st,
+            float* const* dumps = nullptr, int* written = nullptr) {
     if (N != 0 && (!x || !y)) return fail(CNN_ERR_INVALID, "net: null input or output");
     if (n > 4096) return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n);
     std::vector<Plan> plan((size_t)std::max(n, 0));
@@ -309,6 +315,8 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
     size_t split_bytes = 0;
     int rc = plan_net(L, n, N, C, H, W, plan.data(), &mx, true, &split_bytes);
     if (rc) return rc;
+    if (written)
+        for (int i = 0; i < n; ++i) written[i] = 0;
     if (N == 0) {  // nothing to compute; still honour the event contract
         for (int i = 0; events && i <= n; ++i)
             if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), st) != hipSuccess)
@@ -403,6 +411,12 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
                 const FillJobs* fj = i == fill_host ? &host_fills : nullptr;
                 if (p.lrn_from >= 0) {  // cur is still the LRN's input
                     const cnn_layer_desc& ld = L[p.lrn_from];
+                    if (dumps && dumps[p.lrn_from]) {
+                        rc = launch_lrn(cur, N, p.inC, p.inH, p.inW, ld.lrn_size, ld.lrn_alpha, ld.lrn_beta,
+                                        ld.lrn_k, dumps[p.lrn_from], st, relu_in);
+                        if (rc) return fail(rc, "net layer %d: %s", p.lrn_from, std::string(cnn_last_error()).c_str());
+                        if (written) written[p.lrn_from] = 1;
+                    }
                     rc = launch_lrn_pool(p.pool, d.pool_mode, p.relu, ld.lrn_size, ld.lrn_alpha,
                                          ld.lrn_beta, ld.lrn_k, cur, out, d.pool_index, st, relu_in, fj,
                                          p.opad_h, p.opad_w);
@@ -423,6 +437,14 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
                 break;
         }
         if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
+        if (dumps && dumps[i]) {
+            // the stored output without the zero border a pooling layer may give
+            // it, and with a ReLU this layer left to the next one
+            const int bh = p.type == CNN_LAYER_POOL ? p.opad_h : 0, bw = p.type == CNN_LAYER_POOL ? p.opad_w : 0;
+            rc = launch_copy_planes(out, dumps[i], (int64_t)N * p.outC, p.outH, p.outW, bh, bw, relu_pending, st);
+            if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
+            if (written) written[i] = 1;
+        }
         if (out == buf[next_buf]) next_buf ^= 1;
         cur = out;
     }
@@ -553,6 +575,14 @@ int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x
                       cnn_stream_t stream) {
     if (!events) return fail(CNN_ERR_INVALID, "net_fwd_timed: null events");
     return run_net(layers, n_layers, x, N, C, H, W, y, ws, ws_bytes, events, as_stream(stream));
+}
+
+int cnn_net_fwd_dump(const cnn_layer_desc* layers, int n_layers, const float* x, int N, int C, int H,
+                     int W, float* y, void* ws, size_t ws_bytes, float* const* dumps, int* written,
+                     cnn_stream_t stream) {
+    if (!dumps) return fail(CNN_ERR_INVALID, "net_fwd_dump: null dump array");
+    return run_net(layers, n_layers, x, N, C, H, W, y, ws, ws_bytes, nullptr, as_stream(stream), dumps,
+                   written);
 }
 
 }  // extern "C"

@@ -435,7 +435,32 @@ __global__ void __launch_bounds__(kThreads) relu_f32(const float* x, float* y, i
         y[i] = relu1(x[i]);
 }
 
+// ------------------------------------------------------------------ copies
+// dst[plane][p][q] = src[plane][p + bh][q + bw] (source planes of
+// (P + 2 bh) x (Q + 2 bw)), through a ReLU when `relu` is set: the layer
+// outputs a network pass writes out for checking.
+__global__ void __launch_bounds__(kThreads) copy_planes_f32(const float* src, float* dst, int64_t total,
+                                                            int P, int Q, int bh, int bw, int relu) {
+    const int64_t PQ = (int64_t)P * Q, QB = Q + 2 * bw, PQB = (int64_t)(P + 2 * bh) * QB;
+    for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * kThreads) {
+        const int64_t plane = i / PQ, r = i - plane * PQ;
+        const int64_t p = r / Q, q = r - p * Q;
+        const float v = src[plane * PQB + (p + bh) * QB + q + bw];
+        dst[i] = relu ? relu1(v) : v;
+    }
+}
+
 }  // namespace
+
+int launch_copy_planes(const float* src, float* dst, int64_t planes, int P, int Q, int bh, int bw,
+                       bool relu, hipStream_t st) {
+    const int64_t total = planes * P * Q;
+    if (total == 0) return CNN_OK;
+    hipLaunchKernelGGL(copy_planes_f32, dim3(grid_for(total)), dim3(kThreads), 0, st, src, dst, total, P, Q,
+                       bh, bw, (int)relu);
+    return check_launch("copy_planes_f32");
+}
 
 int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y, int32_t* idx,
                 hipStream_t st, bool relu_x, const FillJobs* fills) {

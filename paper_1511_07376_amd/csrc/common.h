@@ -112,5 +112,9 @@ int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alph
                     const float* x, float* y, int32_t* idx, hipStream_t st, bool relu_x = false,
                     const FillJobs* fills = nullptr, int opad_h = 0, int opad_w = 0);
 int launch_softmax(const float* x, int N, int C, int HW, float* y, hipStream_t st);
+// dst [planes][P][Q] = the inner P x Q of src's planes of (P + 2 bh) x
+// (Q + 2 bw), through a ReLU when relu is set.
+int launch_copy_planes(const float* src, float* dst, int64_t planes, int P, int Q, int bh, int bw,
+                       bool relu, hipStream_t st);
 
 }  // namespace cnn

@@ -225,6 +225,9 @@ def test_net_rejects_before_launch():
     assert L.cnn_net_fwd(descs, 0, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, 0) == cnn.CNN_ERR_INVALID
     assert L.cnn_net_fwd(descs, n, FAKE, 2, 4, H, W, FAKE, FAKE, 1 << 40, 0) == cnn.CNN_ERR_INVALID
     assert L.cnn_net_fwd_timed(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, None, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_net_fwd_dump(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, None, None, 0) == \
+        cnn.CNN_ERR_INVALID
+    assert "dump" in cnn.cnn_last_error()
     assert L.cnn_net_workspace_bytes(descs, 0, 2, C, H, W) == 0
 
 

@@ -77,9 +77,46 @@ def test_conv_sweep_batch1(gpu, shape):
 
 
 @pytest.mark.parametrize("shape", wl.SWEEP_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_conv_sweep_batch16_sampled(gpu, shape):
+    C, H, W, K, R, S, st, pd = shape
+    _conv_case(gpu, 16, C, H, W, K, R, S, st, pd, 1, seed=6, sample=[0, 7, 15])
+
+
+@pytest.mark.parametrize("shape", wl.SWEEP_SHAPES, ids=lambda s: "x".join(map(str, s)))
 def test_conv_sweep_batch64_sampled(gpu, shape):
     C, H, W, K, R, S, st, pd = shape
     _conv_case(gpu, 64, C, H, W, K, R, S, st, pd, 1, seed=4, sample=[0, 63])
+
+
+# The five AlexNet conv layers at batch 64 as the network runs them: conv2
+# and conv3 read planes that the LRN + pooling kernel before them wrote
+# inside a zero border of their padding width, and run unpadded on the
+# bordered (H + 2p) x (W + 2p) planes.  (N, C, H, W, K, R, S, stride, pad, G)
+ALEXNET_B64_AS_RUN = [
+    (64, 3, 227, 227, 96, 11, 11, 4, 0, 1),
+    (64, 96, 31, 31, 256, 5, 5, 1, 0, 2),
+    (64, 256, 15, 15, 384, 3, 3, 1, 0, 1),
+    (64, 384, 13, 13, 384, 3, 3, 1, 1, 2),
+    (64, 384, 13, 13, 256, 3, 3, 1, 1, 2),
+]
+
+
+@pytest.mark.parametrize("shape", ALEXNET_B64_AS_RUN, ids=[f"conv{i + 1}" for i in range(5)])
+def test_conv_alexnet_b64_every_config(gpu, shape):
+    """Every tile configuration (and the heuristic) on each AlexNet batch-64
+    conv shape, so that whichever configuration the auto-tuner keeps for the
+    benchmark has been checked at that exact shape; sampled images."""
+    N, C, H, W, K, R, S, st, pd, G = shape
+    x = wl.normal((N, C, H, W), 1.0, 23, 0)
+    w = wl.normal((K, C // G, R, S), 1.0, 23, 1)
+    b = wl.normal((K,), 1.0, 23, 2)
+    rows = [0, 31, 63]
+    ref = oracle.conv2d_fwd(x[rows], w, b, (st, st), (pd, pd), G, True)
+    xd, wd, bd = to_dev(x), to_dev(w), to_dev(b)
+    for cfg in range(-1, gpu.cnn_conv2d_num_configs()):
+        print(f"alexnet b64 conv config {cfg} ({gpu.cnn_conv2d_config_name(cfg)}) shape {shape}", flush=True)
+        y = gpu.cnn_conv2d_fwd(xd, wd, bd, st, pd, G, True, config=cfg)
+        assert_gemm_close(to_host(y)[rows], ref, (C // G) * R * S, f"config {cfg}")
 
 
 # ---------------------------------------------------------------- odd shapes

@@ -10,8 +10,9 @@ pooling kernel, FC chains, a softmax at the end, and batches of 1 (every
 conv and FC layer split across workgroups), 5 and 33 (FC tile geometries on
 both sides of 32 images).
 
-Tolerance: the final output within the FC criterion of the last FC layer
-(Kred = its input features).
+Each pass runs through cnn_net_fwd_dump and every layer is checked
+(tests/netcheck.py): against the oracle's chain and against the oracle's
+layer on the pass's own input of that layer, max-pool indices included.
 """
 import numpy as np
 import pytest
@@ -19,6 +20,7 @@ import pytest
 import oracle
 from conftest import to_dev, to_host
 from paper_1511_07376_amd import workloads as wl
+from netcheck import dump_and_compare
 from parity import assert_gemm_close
 
 N_NETS = 24
@@ -100,14 +102,12 @@ def test_random_nets_are_valid():
 def test_random_net_matches_oracle(gpu, seed):
     net = random_net(seed)
     params = wl.make_params(net, seed)
-    model = gpu.Network(net, params)
+    model = gpu.Network(net, params, pool_index=True)
     kinds = " ".join(l.kind for l in net.layers)
     for batch in BATCHES:
         print(f"random net {seed} ({net.input_chw}: {kinds}) batch {batch}", flush=True)
         x = wl.make_input(net, batch, 100 + seed)
-        y = to_host(model(to_dev(x)))
-        ref = oracle.net_fwd(net, x, params)
-        assert_gemm_close(y.reshape(ref.shape), ref, _last_fc_in(net), f"random{seed} B{batch}")
+        dump_and_compare(gpu, net, params, x, model=model, what=f"random{seed} B{batch}")
 
 
 @pytest.mark.gpu
