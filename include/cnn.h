@@ -245,6 +245,30 @@ int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x
                       int N, int C, int H, int W, float* y, void* ws,
                       size_t ws_bytes, void* const* events, cnn_stream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): cnn_net_fwd
+ * with the library's own static device scratch as the workspace, of
+ * CNN_NOALLOC_SCRATCH_BYTES per GPU (256 MiB: AlexNet-shaped networks up to
+ * batch 64, LeNet and CIFAR-10 quick up to batch 256).
+ *   - Allocates no device memory: no hipMalloc / hipFree, no events or
+ *     streams, and it never runs the auto-tuner (a conv shape the tuner has
+ *     not recorded takes the built-in heuristic).  The scratch is a
+ *     file-scope device array, one copy per GPU, held until the process ends;
+ *     its device address is looked up once per device on the first call
+ *     there.
+ *   - x, y, the layer descriptors and the parameters are the caller's, as for
+ *     cnn_net_fwd; a network whose cnn_net_workspace_bytes() exceeds
+ *     CNN_NOALLOC_SCRATCH_BYTES gets CNN_ERR_WORKSPACE and nothing is
+ *     enqueued.
+ *   - Every call on one GPU uses the same scratch, which keeps the last pass's
+ *     intermediates; a pass writes every intermediate before reading it, so
+ *     nothing needs clearing between calls.  Calls that overlap on one GPU
+ *     (several streams or threads at once) race on the scratch: the caller
+ *     orders them. */
+#define CNN_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+int cnn_net_fwd_noalloc(const cnn_layer_desc* layers, int n_layers, const float* x,
+                        int N, int C, int H, int W, float* y, cnn_stream_t stream);
+
 /* As cnn_net_fwd, and also writes every layer's output, so that each layer of
  * a network pass can be compared with a reference of that layer (the paper
  * checks only the last layer's output, Sec. 4.1).  A checking aid: the copies

@@ -79,6 +79,8 @@ lib.cnn_net_fwd_timed.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes
                                   ctypes.POINTER(ctypes.c_void_p), _p]
 lib.cnn_net_fwd_dump.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
                                  ctypes.POINTER(ctypes.c_void_p), _ip, _p]
+lib.cnn_net_fwd_noalloc.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p]
+CNN_NOALLOC_SCRATCH_BYTES = 256 << 20
 lib.cnn_conv2d_fwd_config.argtypes = lib.cnn_conv2d_fwd.argtypes[:17] + [_i, _p]
 lib.cnn_netfile_parse.argtypes = [ctypes.c_char_p, _descp, _i, _ip, ctypes.POINTER(cnn_netfile_config)]
 lib.cnn_net_graph_create.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
@@ -98,7 +100,8 @@ lib.cnn_version.restype = ctypes.c_char_p
 for _name in ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
               "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_softmax_fwd", "cnn_net_out_shape",
               "cnn_net_fwd",
-              "cnn_net_fwd_timed", "cnn_net_fwd_dump", "cnn_conv2d_fwd_config", "cnn_conv2d_num_configs",
+              "cnn_net_fwd_timed", "cnn_net_fwd_dump", "cnn_net_fwd_noalloc", "cnn_conv2d_fwd_config",
+              "cnn_conv2d_num_configs",
               "cnn_set_autotune", "cnn_tuning_import", "cnn_tuning_clear", "cnn_netfile_parse",
               "cnn_net_graph_create", "cnn_net_graph_launch", "cnn_net_graph_destroy"):
     getattr(lib, _name).restype = _i
@@ -106,7 +109,7 @@ for _name in ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "c
 EXPORTED = ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
             "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_softmax_fwd", "cnn_net_out_shape",
             "cnn_net_workspace_bytes", "cnn_net_fwd", "cnn_net_fwd_timed", "cnn_net_fwd_dump",
-            "cnn_last_error",
+            "cnn_net_fwd_noalloc", "cnn_last_error",
             "cnn_version", "cnn_conv2d_num_configs", "cnn_conv2d_config_name",
             "cnn_conv2d_fwd_config", "cnn_set_autotune", "cnn_tuning_export",
             "cnn_tuning_import", "cnn_tuning_clear", "cnn_netfile_parse", "cnn_net_graph_create",
@@ -551,6 +554,17 @@ class Network:
         return y
 
     __call__ = forward
+
+    def forward_noalloc(self, x: torch.Tensor, y: Optional[torch.Tensor] = None, stream=None):
+        """cnn_net_fwd_noalloc: the pass with the library's static device
+        scratch as its workspace (no workspace tensor is allocated here; y is
+        allocated when None)."""
+        N, C, H, W = x.shape
+        if y is None:
+            y = torch.empty(self.out_shape(N), dtype=torch.float32, device=x.device)
+        _ok(lib.cnn_net_fwd_noalloc(self.descs, len(self.descs), _dev(x, "x"), N, C, H, W, _dev(y, "y"),
+                                    _stream(stream)))
+        return y
 
     def layer_shapes(self, N: int) -> List[Tuple[int, ...]]:
         """Output shape of every layer for a batch of N (the library's shape rules)."""

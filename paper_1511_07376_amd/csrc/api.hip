@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -167,8 +168,11 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 // the outputs of split-reduction conv and FC layers (other than the last
 // layer), which are all set to their biases by one launch at the start of
 // the pass.
+// no_tune: the pass will not run the auto-tuner (shapes without a record take
+// the heuristic).
 int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* plan,
-             int64_t* max_elems, bool need_weights = true, size_t* split_bytes = nullptr) {
+             int64_t* max_elems, bool need_weights = true, size_t* split_bytes = nullptr,
+             bool no_tune = false) {
     if (!L || n <= 0) return fail(CNN_ERR_INVALID, "net: no layers");
     if (N < 0 || C <= 0 || H <= 0 || W <= 0)
         return fail(CNN_ERR_INVALID, "net: input %dx%dx%dx%d", N, C, H, W);
@@ -222,7 +226,7 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
                     // be tuned) splits
                     for (int cfg = 0; cfg < conv2d_num_configs() && !p.may_split; ++cfg)
                         p.may_split = conv2d_splits(p.conv, cfg) > 1;
-                    const int cfg = conv2d_planned_config(p.conv);
+                    const int cfg = conv2d_planned_config(p.conv, no_tune);
                     p.split = cfg != -2 && conv2d_splits(p.conv, cfg) > 1;
                     p.may_split = p.may_split || p.split;
                 }
@@ -305,15 +309,16 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
 // = 0) for a RELU layer executed inside its predecessor, whose dump then holds
 // the output after that ReLU.  An LRN run inside the pooling layer after it is
 // also run on its own into its dump (the fused kernel never stores it).
+// no_tune: never run the auto-tuner in this pass.
 int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H, int W, float* y,
             void* ws, size_t ws_bytes, void* const* events, hipStream_t st,
-            float* const* dumps = nullptr, int* written = nullptr) {
+            float* const* dumps = nullptr, int* written = nullptr, bool no_tune = false) {
     if (N != 0 && (!x || !y)) return fail(CNN_ERR_INVALID, "net: null input or output");
     if (n > 4096) return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n);
     std::vector<Plan> plan((size_t)std::max(n, 0));
     int64_t mx = 0;
     size_t split_bytes = 0;
-    int rc = plan_net(L, n, N, C, H, W, plan.data(), &mx, true, &split_bytes);
+    int rc = plan_net(L, n, N, C, H, W, plan.data(), &mx, true, &split_bytes, no_tune);
     if (rc) return rc;
     if (written)
         for (int i = 0; i < n; ++i) written[i] = 0;
@@ -397,6 +402,7 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
         switch (p.type) {
             case CNN_LAYER_CONV: {
                 ConvOpts o;
+                o.no_tune = no_tune;
                 o.relu_in = relu_in;
                 o.prefilled = p.split;
                 o.relu_left = relu_left;
@@ -452,6 +458,43 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
         if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[n]), st) != hipSuccess)
             return check_launch("hipEventRecord");
     }
+    return CNN_OK;
+}
+
+// ------------------------------------------------------------------ static scratch
+// The workspace of cnn_net_fwd_noalloc: a device array of the library's own,
+// one copy per GPU (allocated when the code object is loaded on that GPU and
+// held until the process ends).  Host code never uses the array's name as an
+// address: the device address of each GPU's copy is taken once, with that
+// GPU current, and kept per device.
+constexpr size_t kScratchBytes = CNN_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxScratchDevices] = {};
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+// Device address of the current device's copy of `scratch`.
+int scratch_of_current_device(void** addr) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return check_launch("hipGetDevice");
+    if (dev < 0 || dev >= kMaxScratchDevices)
+        return fail(CNN_ERR_UNSUPPORTED, "net_fwd_noalloc: device %d beyond the %d supported", dev,
+                    kMaxScratchDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(CNN_ERR_HIP, "net_fwd_noalloc: hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                        hipGetErrorString(e));
+        g_scratch_addr[dev] = p;
+    }
+    *addr = g_scratch_addr[dev];
     return CNN_OK;
 }
 
@@ -575,6 +618,29 @@ int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x
                       cnn_stream_t stream) {
     if (!events) return fail(CNN_ERR_INVALID, "net_fwd_timed: null events");
     return run_net(layers, n_layers, x, N, C, H, W, y, ws, ws_bytes, events, as_stream(stream));
+}
+
+int cnn_net_fwd_noalloc(const cnn_layer_desc* layers, int n_layers, const float* x, int N, int C, int H,
+                        int W, float* y, cnn_stream_t stream) {
+    if (n_layers > 4096) return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n_layers);
+    std::vector<Plan> plan((size_t)std::max(n_layers, 0));
+    int64_t mx = 0;
+    size_t split_bytes = 0;
+    int rc = plan_net(layers, n_layers, N, C, H, W, plan.data(), &mx, true, &split_bytes, true);
+    if (rc) return rc;
+    const size_t need = 2 * align_up((size_t)mx * sizeof(float)) + split_bytes;
+    if (need > kScratchBytes)
+        return fail(CNN_ERR_WORKSPACE,
+                    "net_fwd_noalloc: this input needs %zu bytes of workspace, the static scratch holds %zu "
+                    "(use cnn_net_fwd with a workspace of cnn_net_workspace_bytes())",
+                    need, kScratchBytes);
+    void* ws = nullptr;
+    if (N > 0) {
+        rc = scratch_of_current_device(&ws);
+        if (rc) return rc;
+    }
+    return run_net(layers, n_layers, x, N, C, H, W, y, ws, kScratchBytes, nullptr, as_stream(stream), nullptr,
+                   nullptr, true);
 }
 
 int cnn_net_fwd_dump(const cnn_layer_desc* layers, int n_layers, const float* x, int N, int C, int H,

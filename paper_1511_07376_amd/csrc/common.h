@@ -44,10 +44,14 @@ int pool_out(int H, int W, int kh, int kw, int sh, int sw, int ph, int pw, int c
 //   prefilled y already holds the bias (only with a split reduction);
 //   relu_left non-null: a ReLU that would need a pass of its own (split
 //             reduction) is skipped and *relu_left set, for the consumer.
+//   no_tune   never run the auto-tuner for this call (a shape without a
+//             record takes the heuristic), as for a caller that must not
+//             allocate or synchronise.
 struct ConvOpts {
     bool relu_in = false;
     bool prefilled = false;
     bool* relu_left = nullptr;
+    bool no_tune = false;
 };
 // cfg: index into the convolution configuration table, or -1 for the
 // built-in heuristic.
@@ -62,8 +66,9 @@ int conv2d_splits(const ConvShape& s, int cfg);
 int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const float* bias,
                     int relu, float* y, hipStream_t st, const ConvOpts* opt = nullptr);
 // The configuration conv2d_dispatch would use now: the tuned one, else the
-// heuristic (-1); -2 when the shape would be auto-tuned first.
-int conv2d_planned_config(const ConvShape& s);
+// heuristic (-1); -2 when the shape would be auto-tuned first (never with
+// no_tune).
+int conv2d_planned_config(const ConvShape& s, bool no_tune = false);
 // relu_in: apply a ReLU to x as it is read.  relu_left non-null: when the
 // layer's ReLU would need a pass of its own (split reduction), skip it and set
 // *relu_left, so that the caller can fold it into the next layer's input.

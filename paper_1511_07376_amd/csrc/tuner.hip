@@ -92,11 +92,11 @@ int tune(const ConvShape& s, const float* x, const float* w, const float* bias, 
 
 }  // namespace
 
-int conv2d_planned_config(const ConvShape& s) {
+int conv2d_planned_config(const ConvShape& s, bool no_tune) {
     std::lock_guard<std::mutex> lock(g_mu);
     auto it = g_table.find(key_of(s));
     if (it != g_table.end()) return it->second;
-    return g_autotune ? -2 : -1;
+    return g_autotune && !no_tune ? -2 : -1;
 }
 
 int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const float* bias, int relu,
@@ -109,7 +109,7 @@ int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const fl
         if (it != g_table.end()) cfg = it->second;
         autotune = g_autotune != 0;
     }
-    if (cfg < 0 && autotune && s.N > 0) {
+    if (cfg < 0 && autotune && s.N > 0 && !(opt && opt->no_tune)) {
         cfg = tune(s, x, w, bias, relu, y, st);
         if (cfg >= 0) {
             std::lock_guard<std::mutex> lock(g_mu);

@@ -228,6 +228,12 @@ def test_net_rejects_before_launch():
     assert L.cnn_net_fwd_dump(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, None, None, 0) == \
         cnn.CNN_ERR_INVALID
     assert "dump" in cnn.cnn_last_error()
+    # the no-allocation pass: validated like cnn_net_fwd, and a workspace
+    # beyond the static scratch is refused before any device call
+    assert L.cnn_net_fwd_noalloc(descs, 0, FAKE, 2, C, H, W, FAKE, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_net_workspace_bytes(descs, n, 128, C, H, W) > cnn.CNN_NOALLOC_SCRATCH_BYTES
+    assert L.cnn_net_fwd_noalloc(descs, n, FAKE, 128, C, H, W, FAKE, 0) == cnn.CNN_ERR_WORKSPACE
+    assert "static scratch" in cnn.cnn_last_error()
     assert L.cnn_net_workspace_bytes(descs, 0, 2, C, H, W) == 0
 
 
