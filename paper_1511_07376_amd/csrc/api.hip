@@ -207,7 +207,8 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
                     ConvShape bordered;
                     const int64_t hb64 = (int64_t)h + 2 * (int64_t)d.pad_h, wb64 = (int64_t)w + 2 * (int64_t)d.pad_w;
                     const int hb = (int)std::min<int64_t>(hb64, INT32_MAX), wb = (int)std::min<int64_t>(wb64, INT32_MAX);
-                    if (hb64 <= INT32_MAX && wb64 <= INT32_MAX &&
+                    // (the pooling kernel's bordered output planes stay below 2^24 elements)
+                    if (hb64 < ((int64_t)1 << 24) && wb64 < ((int64_t)1 << 24) && hb64 * wb64 < ((int64_t)1 << 24) &&
                         check_conv(N, c, hb, wb, d.out_channels, d.kernel_h, d.kernel_w, d.stride_h,
                                    d.stride_w, 0, 0, d.groups, &bordered) == CNN_OK &&
                         bordered.P == p.conv.P && bordered.Q == p.conv.Q) {

@@ -33,8 +33,44 @@ struct PoolParams {
     int total;  // N*C*P*Q
     int relu;
     int relu_x;  // take the input through a ReLU as it is read
+    int inside;  // no padding and every window lies inside the plane
     FillJobs fills;  // bias fills run after the pooling (n = 0: none)
 };
+
+// One pooling window whose KH x KW taps all lie inside the plane (no padding,
+// no clipping): t points at its top-left element, ld is the row pitch.  The
+// order and the comparisons are those of the clipped loops of the kernels
+// below, so the bits are the same: the first maximum in row-major order
+// (*rel = its row * ld + column offset from t), or the row-major sum from 0
+// (the caller divides by KH * KW, the count of the clipped rule).
+template <int MODE, int KH, int KW>
+__device__ inline float pool_inside(const float* t, int ld, int* rel) {
+    if constexpr (MODE == 0) {
+        float best = t[0];
+        int bi = 0;
+#pragma unroll
+        for (int dh = 0; dh < KH; ++dh)
+#pragma unroll
+            for (int dw = 0; dw < KW; ++dw) {
+                if (dh == 0 && dw == 0) continue;
+                const float v = t[dh * ld + dw];
+                if (v > best) {
+                    best = v;
+                    bi = dh * ld + dw;
+                }
+            }
+        *rel = bi;
+        return best;
+    } else {
+        float sum = 0.0f;
+#pragma unroll
+        for (int dh = 0; dh < KH; ++dh)
+#pragma unroll
+            for (int dw = 0; dw < KW; ++dw) sum += t[dh * ld + dw];
+        *rel = 0;
+        return sum;
+    }
+}
 
 template <bool WITH_IDX>
 __global__ void __launch_bounds__(kThreads) maxpool_f32(PoolParams p) {
@@ -121,6 +157,23 @@ pool_staged_f32(PoolParams p, int planes_per_block, int nplanes, FastDiv fpq, Fa
         }
         __syncthreads();
         const int outs = np * PQ;
+        if (KH > 0 && p.inside) {  // uniform: windows need no clipping
+            for (int o = threadIdx.x; o < outs; o += kThreads) {
+                const int pl = (int)fdiv(o, fpq);
+                const int r = o - pl * PQ;
+                const int pp = (int)fdiv(r, fq);
+                const int q = r - pp * p.Q;
+                const int corner = pp * sh * p.W + q * sw;
+                int rel;
+                float out = pool_inside<MODE, KH ? KH : 1, KW ? KW : 1>(tile + pl * HW + corner, p.W, &rel);
+                if constexpr (MODE == 1) out = out / (float)(kh * kw);
+                if (WITH_IDX && MODE == 0) p.idx[(size_t)pl0 * PQ + o] = corner + rel;
+                if (p.relu) out = out > 0.0f ? out : 0.0f;
+                p.y[(size_t)pl0 * PQ + o] = out;
+            }
+            __syncthreads();
+            continue;
+        }
         for (int o = threadIdx.x; o < outs; o += kThreads) {
             const int pl = (int)fdiv(o, fpq);
             const int r = o - pl * PQ;
@@ -257,36 +310,45 @@ __global__ void __launch_bounds__(kThreads) lrn_across_f32(LrnParams p) {
 
 // LRN followed by pooling in one pass, for the network executor (an LRN layer
 // whose output only feeds a pooling layer): the LRN output never goes to
-// memory.  A workgroup takes one image, CB channels and a band of PB pooling
+// memory.  A workgroup takes one image, CC channels and a band of PB pooling
 // output rows (RB input rows):
-//   1. each work-item is one pixel of the band and CC consecutive channels:
-//      it loads those channels plus the HALF-channel halo on each side
-//      straight into registers (every load in flight at once; channels and
-//      rows outside the tensor read 0) and writes the CC LRN values to LDS,
-//      with the same arithmetic as the LRN kernel;
+//   1. each work-item is one pixel of the band: it loads its CC channels plus
+//      the HALF-channel halo on each side straight into registers (every load
+//      in flight at once; channels and rows outside the tensor read 0) and
+//      writes the CC LRN values to LDS, with the same arithmetic as the LRN
+//      kernel;
 //   2. pools from the LDS tile (same order and comparisons as the pooling
 //      kernels), so the result equals the two layers run one after the other,
 //      bit for bit.
+// The channel chunk is uniform over the workgroup, so the channel part of
+// each load offset is a scalar and a channel outside the tensor is a
+// workgroup-wide decision.  Planes (input, LDS band, output) are below 2^24
+// elements (checked on the host), so the index arithmetic uses 24-bit
+// multiplies.
 struct LrnPoolParams {
     const float* x;
     float* y;
     int32_t* idx;
     int C, H, W, P, Q, kh, kw, sh, sw, ph, pw;
-    int CB, PB, RB;   // channels, output rows and input rows per workgroup
+    int PB, RB;       // output rows and input rows per workgroup
     int nchunk, nband;
     int relu_x;       // take the input through a ReLU as it is read
-    FastDiv f_plane, f_w, f_pbq, f_q;  // RB*W, W, PB*OQ, OQ (OQ = Q + 2 opad_w)
+    FastDiv f_pbq, f_q;  // PB*OQ, OQ (OQ = Q + 2 opad_w)
     int relu;
     float alpha_over_size, beta, k;
     int opad_h, opad_w;  // y holds each plane inside a zero border of this width
     FillJobs fills;      // bias fills run after the pooling (n = 0: none)
 };
 
-template <int HALF, int CC, int MODE, bool WITH_IDX>  // MODE 0: max, 1: average
+__device__ inline int mul24(int a, int b) { return (int)__umul24((unsigned)a, (unsigned)b); }
+
+// KWIN = 3: 3x3 windows of stride 2 that all lie inside the plane (no
+// padding), taken with constant offsets; 0: any window, clipped.
+template <int HALF, int CC, int MODE, bool WITH_IDX, int KWIN>  // MODE 0: max, 1: average
 __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
     constexpr int WIN = 2 * HALF + 1;
     constexpr int NV = CC + 2 * HALF;       // channels loaded per work-item
-    extern __shared__ float lrn[];          // [CB][RB][W]
+    extern __shared__ float lrn[];          // [CC][RB][W]
     // Workgroups go to the 8 XCDs in turn by id, each XCD with its own L2.
     // Neighbouring channel chunks read the same halo channels, so the ids
     // are remapped to give each XCD a contiguous run of (image, band, chunk)
@@ -300,61 +362,70 @@ __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
     b /= p.nchunk;
     const int band = b % p.nband;
     const int n = b / p.nband;
-    const int c0 = chunk * p.CB;
+    const int c0 = chunk * CC;
     const int p0 = band * p.PB;
     const int pend = min(p0 + p.PB, p.P);
     const int row0 = p0 * p.sh - p.ph;  // first input row of the band (may be < 0)
     const int HW = p.H * p.W;
     const int plane = p.RB * p.W;
 
-    // 1. LRN of the band: work-item (s, r, w) is channels c0 + s CC .. + CC - 1
-    //    at input row row0 + r, column w
+    // 1. LRN of the band: work-item `it` is the pixel row0 * W + it of the
+    //    image (rows outside the image read 0), channels c0 .. c0 + CC - 1
     const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(p.x + (size_t)n * p.C * HW), (short)0, 0x7fffffff, 0x00020000);
-    const int nitem = (p.CB / CC) * plane;
-    for (int it = threadIdx.x; it < nitem; it += kThreads) {
-        const int s = (int)fdiv(it, p.f_plane);
-        const int rw = it - s * plane;
-        const int r = (int)fdiv(rw, p.f_w);
-        const int h = row0 + r;
-        const int pix = h * p.W + (rw - r * p.W);
-        const int cs = c0 + s * CC - HALF;  // channel of v[0]
-        const bool hok = (unsigned)h < (unsigned)p.H;
+    const int cs = c0 - HALF;  // channel of v[0]
+    const int hw4 = HW * 4;
+    for (int it = threadIdx.x; it < plane; it += kThreads) {
+        const int pix = row0 * p.W + it;
+        const int lane_off = (unsigned)pix < (unsigned)HW ? pix * 4 : (int)0x80000000u;
         float v[NV];
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
-            const int c = cs + j;
-            const int off = hok && (unsigned)c < (unsigned)p.C ? (c * HW + pix) * 4 : (int)0x80000000u;
-            v[j] = relu_in(__builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0)),
-                           p.relu_x);
+            const int c = cs + j;  // uniform
+            const int off = (unsigned)c < (unsigned)p.C ? lane_off + c * hw4 : (int)0x80000000u;
+            v[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0));
         }
-        float* out = lrn + s * CC * plane + rw;
+        if (p.relu_x) {  // uniform
+#pragma unroll
+            for (int j = 0; j < NV; ++j) v[j] = relu_in(v[j], 1);
+        }
+        float* out = lrn + it;
 #pragma unroll
         for (int i = 0; i < CC; ++i) out[i * plane] = lrn_value<WIN>(&v[i], p.k, p.alpha_over_size, p.beta);
     }
     __syncthreads();
 
-    // 3. pooling from the LRN tile.  Work-item (c, pr, qq) is column qq of
+    // 2. pooling from the LRN tile.  Work-item (c, pr, qq) is column qq of
     //    y's row for output row p0 + pr, border columns included, so that
     //    every row of y is written whole (border columns get 0).
     const int PQ = p.P * p.Q;
     const int OQ = p.Q + 2 * p.opad_w, OPQ = (p.P + 2 * p.opad_h) * OQ;  // y's plane
     const int pbq = p.PB * OQ;
-    const int nout = p.CB * pbq;
+    const int nout = CC * pbq;
+    const int nc0 = n * p.C + c0;  // first (image, channel) plane of the workgroup
+    float* yw = p.y + (size_t)nc0 * OPQ + (size_t)(p0 + p.opad_h) * OQ;
     for (int o = threadIdx.x; o < nout; o += kThreads) {
         const int c = (int)fdiv(o, p.f_pbq);
-        const int rq = o - c * pbq;
+        const int rq = o - mul24(c, pbq);
         const int pr = (int)fdiv(rq, p.f_q);
-        const int qq = rq - pr * OQ;
+        const int qq = rq - mul24(pr, OQ);
         const int pp = p0 + pr;
         if (c0 + c >= p.C || pp >= pend) continue;
         const int q = qq - p.opad_w;
         float out = 0.0f;
-        if ((unsigned)q < (unsigned)p.Q) {
+        if (KWIN == 3 && (unsigned)q < (unsigned)p.Q) {
+            const int hs = pp * 2, ws = q * 2;
+            int rel;
+            out = pool_inside<MODE, 3, 3>(lrn + mul24(c, plane) + mul24(hs - row0, p.W) + ws, p.W, &rel);
+            if constexpr (MODE == 1) out = out / 9.0f;
+            if (WITH_IDX && MODE == 0)
+                p.idx[(size_t)(nc0 + c) * PQ + mul24(pp, p.Q) + q] = mul24(hs, p.W) + ws + rel;
+            if (p.relu) out = out > 0.0f ? out : 0.0f;
+        } else if ((unsigned)q < (unsigned)p.Q) {
             const int hs = pp * p.sh - p.ph, ws = q * p.sw - p.pw;
             const int h0 = max(hs, 0), w0 = max(ws, 0);
             const int h1 = min(hs + p.kh, p.H), w1 = min(ws + p.kw, p.W);
-            const float* t = lrn + c * plane;
+            const float* t = lrn + mul24(c, plane);
             if constexpr (MODE == 0) {
                 int bi = h0 * p.W + w0;  // first maximum in row-major order
                 float best = t[(h0 - row0) * p.W + w0];
@@ -367,7 +438,7 @@ __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
                         }
                     }
                 out = best;
-                if (WITH_IDX) p.idx[(size_t)(n * p.C + c0 + c) * PQ + pp * p.Q + q] = bi;
+                if (WITH_IDX) p.idx[(size_t)(nc0 + c) * PQ + pp * p.Q + q] = bi;
             } else {
                 const int count = (min(hs + p.kh, p.H + p.ph) - hs) * (min(ws + p.kw, p.W + p.pw) - ws);
                 float sum = 0.0f;
@@ -377,20 +448,20 @@ __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
             }
             if (p.relu) out = out > 0.0f ? out : 0.0f;
         }
-        p.y[(size_t)(n * p.C + c0 + c) * OPQ + (pp + p.opad_h) * OQ + qq] = out;
+        yw[mul24(c, OPQ) + rq] = out;
     }
 
-    // 4. y's border rows above the first band and below the last, whole rows
+    // 3. y's border rows above the first band and below the last, whole rows
     if (p.opad_h > 0 && (p0 == 0 || pend == p.P)) {
         const int per_c = p.opad_h * OQ;  // border elements above (or below) a plane
         const int nedge = (p0 == 0) + (pend == p.P);
-        for (int o = threadIdx.x; o < p.CB * nedge * per_c; o += kThreads) {
+        for (int o = threadIdx.x; o < CC * nedge * per_c; o += kThreads) {
             const int ce = o / per_c;  // (channel, edge)
             const int e = o - ce * per_c;
             const int c = ce / nedge;
             const bool below = (ce - c * nedge) == 1 || p0 != 0;
             const int off = below ? (p.opad_h + p.P) * OQ + e : e;
-            if (c0 + c < p.C) p.y[(size_t)(n * p.C + c0 + c) * OPQ + off] = 0.0f;
+            if (c0 + c < p.C) p.y[(size_t)(nc0 + c) * OPQ + off] = 0.0f;
         }
     }
     run_fills(p.fills);
@@ -475,6 +546,8 @@ int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y
     p.kh = s.kh; p.kw = s.kw; p.sh = s.sh; p.sw = s.sw; p.ph = s.ph; p.pw = s.pw;
     p.total = s.N * s.C * s.P * s.Q;
     p.relu = relu;
+    p.inside = s.ph == 0 && s.pw == 0 && (int64_t)(s.P - 1) * s.sh + s.kh <= s.H &&
+               (int64_t)(s.Q - 1) * s.sw + s.kw <= s.W;
     if (p.total == 0) return fills ? launch_bias_fills(fills->job, fills->n, st) : CNN_OK;
     const int plane_bytes = s.H * s.W * 4;
     if (plane_bytes <= kPoolLdsBytes) {
@@ -612,8 +685,10 @@ bool lrn_pool_tiling(const PoolShape& s, int half, LrnPoolTiling* t) {
 
 bool lrn_pool_fusable(const PoolShape& s, int size) {
     LrnPoolTiling t;
+    // the kernel's 24-bit index products: input and output planes below
+    // 2^24 elements (a bordered output plane is checked by the caller)
     if (size % 2 != 1 || size / 2 > 4 || (int64_t)s.C * s.H * s.W >= ((int64_t)1 << 29) ||
-        !lrn_pool_tiling(s, size / 2, &t))
+        (int64_t)s.H * s.W >= ((int64_t)1 << 24) || !lrn_pool_tiling(s, size / 2, &t))
         return false;
     return t.blocks * kThreads < ((int64_t)1 << 32);  // the launch's work-items fit 32 bits
 }
@@ -626,19 +701,20 @@ int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alph
     LrnPoolTiling t;
     if (!lrn_pool_fusable(s, size) || !lrn_pool_tiling(s, half, &t))
         return fail(CNN_ERR_UNSUPPORTED, "lrn+pool: no fused tiling for this shape");
+    const int64_t ohb = (int64_t)s.P + 2 * (int64_t)opad_h, owb = (int64_t)s.Q + 2 * (int64_t)opad_w;
+    if (opad_h < 0 || opad_w < 0 || ohb >= ((int64_t)1 << 24) || owb >= ((int64_t)1 << 24) ||
+        ohb * owb >= ((int64_t)1 << 24))
+        return fail(CNN_ERR_UNSUPPORTED, "lrn+pool: bordered output plane of 2^24 elements or more");
     LrnPoolParams p;
     p.x = x;
     p.y = y;
     p.idx = idx;
     p.C = s.C; p.H = s.H; p.W = s.W; p.P = s.P; p.Q = s.Q;
     p.kh = s.kh; p.kw = s.kw; p.sh = s.sh; p.sw = s.sw; p.ph = s.ph; p.pw = s.pw;
-    p.CB = t.CB;
     p.PB = t.PB;
     p.RB = t.RB;
-    p.nchunk = ceil_div(s.C, p.CB);
+    p.nchunk = ceil_div(s.C, t.CB);
     p.nband = ceil_div(s.P, p.PB);
-    p.f_plane = make_fastdiv(p.RB * s.W);
-    p.f_w = make_fastdiv(s.W);
     p.f_pbq = make_fastdiv(p.PB * (s.Q + 2 * opad_w));  // y's rows hold the border columns too
     p.f_q = make_fastdiv(s.Q + 2 * opad_w);
     p.relu = relu;
@@ -650,30 +726,39 @@ int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alph
     p.opad_w = opad_w;
     p.fills.n = 0;
     if (fills) p.fills = *fills;
-    const size_t shm = (size_t)p.CB * p.RB * s.W * 4;
+    const size_t shm = (size_t)t.CB * p.RB * s.W * 4;
     const dim3 grid((unsigned)t.blocks), block(kThreads);
-#define CNN_LRN_POOL_CC(H, CC)                                                                   \
-    do {                                                                                         \
-        if (mode == CNN_POOL_MAX && idx)                                                         \
-            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 0, true>), grid, block, shm, st, p);         \
-        else if (mode == CNN_POOL_MAX)                                                           \
-            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 0, false>), grid, block, shm, st, p);        \
-        else                                                                                     \
-            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 1, false>), grid, block, shm, st, p);        \
+    // 3x3 windows of stride 2 inside the plane (AlexNet's pooling) take the
+    // constant-offset window for the five-channel LRN
+    const bool win3 = half == 2 && s.kh == 3 && s.kw == 3 && s.sh == 2 && s.sw == 2 && s.ph == 0 &&
+                      s.pw == 0 && (s.P - 1) * 2 + 3 <= s.H && (s.Q - 1) * 2 + 3 <= s.W;
+#define CNN_LRN_POOL_CC(H, CC, KW)                                                                   \
+    do {                                                                                             \
+        if (mode == CNN_POOL_MAX && idx)                                                             \
+            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 0, true, KW>), grid, block, shm, st, p);         \
+        else if (mode == CNN_POOL_MAX)                                                               \
+            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 0, false, KW>), grid, block, shm, st, p);        \
+        else                                                                                         \
+            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 1, false, KW>), grid, block, shm, st, p);        \
     } while (0)
-#define CNN_LRN_POOL(H)                  \
-    do {                                 \
-        if (t.CC == 16)                  \
-            CNN_LRN_POOL_CC(H, 16);      \
-        else                             \
-            CNN_LRN_POOL_CC(H, 8);       \
+#define CNN_LRN_POOL(H, KW)                  \
+    do {                                     \
+        if (t.CC == 16)                      \
+            CNN_LRN_POOL_CC(H, 16, KW);      \
+        else                                 \
+            CNN_LRN_POOL_CC(H, 8, KW);       \
     } while (0)
     switch (half) {
-        case 0: CNN_LRN_POOL(0); break;
-        case 1: CNN_LRN_POOL(1); break;
-        case 2: CNN_LRN_POOL(2); break;
-        case 3: CNN_LRN_POOL(3); break;
-        default: CNN_LRN_POOL(4); break;
+        case 0: CNN_LRN_POOL(0, 0); break;
+        case 1: CNN_LRN_POOL(1, 0); break;
+        case 2:
+            if (win3)
+                CNN_LRN_POOL(2, 3);
+            else
+                CNN_LRN_POOL(2, 0);
+            break;
+        case 3: CNN_LRN_POOL(3, 0); break;
+        default: CNN_LRN_POOL(4, 0); break;
     }
 #undef CNN_LRN_POOL
 #undef CNN_LRN_POOL_CC
