@@ -231,6 +231,100 @@ def conv_shapes(net, batch, cnn):
     return out
 
 
+def single_layer(args):
+    """One conv or FC layer of the network on its own, as the network runs it
+    (a padded conv after an LRN + pooling pair reads bordered planes and runs
+    unpadded, as the network executor arranges), called `--steps` times with
+    HIP events around each call and, with --flush-mb, a read-only sweep of
+    that many MiB before each call, so that no earlier kernel's cached or
+    dirty lines are charged to it (counter runs of one kernel).  One JSON
+    line."""
+    import torch
+    from paper_1511_07376_amd import cnn
+    from paper_1511_07376_amd import workloads as wl
+
+    net = wl.NETS[args.net]
+    batch = args.batch or (64 if args.net == "alexnet" else net.default_batch)
+    c, h, w = net.input_chw
+    counts, found = {}, None
+    layers = list(net.layers)
+    for i, layer in enumerate(layers):
+        counts[layer.kind] = counts.get(layer.kind, 0) + 1
+        name = f"{layer.kind}{counts[layer.kind]}"
+        if layer.kind == "conv":
+            p_, q_ = cnn.cnn_conv2d_out_shape(h, w, *layer.kernel, layer.stride, layer.pad)
+            bordered = (max(layer.pad) > 0 and i >= 2 and layers[i - 1].kind == "pool"
+                        and layers[i - 2].kind == "lrn")
+            if name == args.single_layer:
+                found = (layer, c, h, w, bordered)
+            c, h, w = layer.out_channels, p_, q_
+        elif layer.kind == "pool":
+            h, w = cnn.cnn_pool_out_shape(h, w, layer.kernel, layer.stride, layer.pad, layer.ceil)
+        elif layer.kind == "fc":
+            if name == args.single_layer:
+                found = (layer, c * h * w, 1, 1, False)
+            c, h, w = layer.out_features, 1, 1
+    if found is None:
+        raise SystemExit(f"bench: no conv or fc layer {args.single_layer!r} in {net.name}")
+    layer, c, h, w, bordered = found
+    if args.tuning_file and os.path.exists(args.tuning_file):
+        with open(args.tuning_file) as f:
+            cnn.cnn_tuning_import(f.read())
+    gen = torch.Generator(device="cuda").manual_seed(args.seed)
+    if layer.kind == "conv":
+        pad = (0, 0) if bordered else layer.pad
+        hh, ww = (h + 2 * layer.pad[0], w + 2 * layer.pad[1]) if bordered else (h, w)
+        x = torch.rand((batch, c, hh, ww), device="cuda", generator=gen)
+        wt = torch.randn((layer.out_channels, c // layer.groups) + tuple(layer.kernel), device="cuda",
+                         generator=gen) * 0.01
+        b = torch.randn(layer.out_channels, device="cuda", generator=gen) * 0.01
+        p_, q_ = cnn.cnn_conv2d_out_shape(hh, ww, *layer.kernel, layer.stride, pad)
+        y = torch.empty((batch, layer.out_channels, p_, q_), device="cuda")
+        flops = 2.0 * batch * layer.out_channels * p_ * q_ * (c // layer.groups) * layer.kernel[0] * layer.kernel[1]
+        byts = 4.0 * (x.numel() + y.numel())
+        shape = {"N": batch, "C": c, "H": hh, "W": ww, "K": layer.out_channels, "R": layer.kernel[0],
+                 "S": layer.kernel[1], "stride": list(layer.stride), "pad": list(pad), "groups": layer.groups}
+        call = lambda: cnn.cnn_conv2d_fwd(x, wt, b, layer.stride, pad, layer.groups, layer.relu, y=y)  # noqa: E731
+    else:
+        x = torch.rand((batch, c), device="cuda", generator=gen)
+        wt = torch.randn((layer.out_features, c), device="cuda", generator=gen) * 0.01
+        b = torch.randn(layer.out_features, device="cuda", generator=gen) * 0.01
+        y = torch.empty((batch, layer.out_features), device="cuda")
+        flops = 2.0 * batch * c * layer.out_features
+        byts = 4.0 * (x.numel() + y.numel() + wt.numel())
+        shape = {"N": batch, "I": c, "O": layer.out_features}
+        call = lambda: cnn.cnn_fc_fwd(x, wt, b, layer.relu, y=y)  # noqa: E731
+    flush = torch.ones(args.flush_mb * (1 << 18), device="cuda") if args.flush_mb else None
+    if args.autotune and not args.tuning_file:
+        cnn.cnn_set_autotune(True)
+    for _ in range(max(args.warmup, 1)):
+        call()
+    cnn.cnn_set_autotune(False)
+    if flush is not None:
+        flush.max()
+        flush.max()  # a sweep over clean caches: its own traffic, for counter runs
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(args.steps):
+        if flush is not None:
+            flush.max()  # reads every line of the buffer
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        call()
+        e1.record()
+        times.append((e0, e1))
+    torch.cuda.synchronize()
+    us = [a.elapsed_time(b_) * 1e3 for a, b_ in times]
+    mean = float(np.mean(us))
+    rec = {"single_layer": args.single_layer, "net": net.name, "bordered_input": bordered, "shape": shape,
+           "flush_mb": args.flush_mb, "steps": args.steps, "us_mean": round(mean, 2),
+           "us_median": round(float(np.median(us)), 2), "gflop": round(flops / 1e9, 4),
+           "tflops": round(flops / mean / 1e6, 2), "frac_fp32_mfma": round(flops / mean / 1e6 / PEAK_FP32_MFMA_TFLOPS, 4),
+           "algorithmic_mbytes": round(byts / 1e6, 2),
+           "tuning": cnn.cnn_tuning_export().strip()}
+    print(json.dumps(rec), flush=True)
+
+
 def gemm_reference(args):
     """Each conv layer of the network beside torch's fp32 batched GEMM on the
     same contraction with the im2col matrix already unrolled in memory (so the
@@ -319,6 +413,12 @@ def main():
                     help="run the timed steps round-robin on this many streams, each with its own replica "
                          "of the network (own workspace), so that consecutive passes overlap: serving "
                          "throughput rather than one pass after another")
+    ap.add_argument("--single-layer", default=None, metavar="NAME",
+                    help="instead of the network: time one conv or fc layer of it (conv1, fc2, ...) as the "
+                         "network runs it, one JSON line")
+    ap.add_argument("--flush-mb", type=int, default=0, metavar="MIB",
+                    help="read a buffer of MIB MiB before each timed call (--single-layer) or before each "
+                         "step of the per-layer event pass, so that caches start cold")
     ap.add_argument("--gemm-reference", action="store_true",
                     help="instead of the network: time each conv layer beside torch's fp32 batched GEMM "
                          "on its contraction with the im2col matrix precomputed, one JSON line per layer")
@@ -335,6 +435,8 @@ def main():
         return conv_sweep(args)
     if args.gemm_reference:
         return gemm_reference(args)
+    if args.single_layer:
+        return single_layer(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the images of a batch are independent: on N GPUs each would run batch/N)",
@@ -421,9 +523,12 @@ def main():
     # per-layer region: K more steps with HIP events recorded on the launch
     # stream between the layers (cnn_net_fwd_timed); the event records add a
     # few microseconds per layer, so this region is not used for `value`
+    flush = torch.ones(args.flush_mb * (1 << 18), device="cuda") if args.flush_mb else None
     torch.cuda.synchronize()
     start.record()
     for k in range(args.steps):
+        if flush is not None:
+            flush.max()  # cold caches for this step's layers (outside their events)
         model(xd, y=yd, events=events[k])
     end.record()
     torch.cuda.synchronize()
@@ -489,6 +594,7 @@ def main():
         "conv_ms": round(conv_ms, 5),
         "ms_per_step_with_layer_events": round(ms_step_events, 4),
         "ms_per_step_with_layer_events_median": round(float(np.median(step_ms_events)), 4),
+        "layer_events_after_flush_mb": args.flush_mb,
         "graph_replay": bool(graph is not None),
         "streams": args.streams if graph is None else 1,
         "autotune": bool(args.autotune),
