@@ -496,29 +496,40 @@ conv2d_igemm_f32(ConvParams p) {
                         acc[i][j][v] += smem[((q - 1) * E + (i * FN + j) * 16 + v) * NT + tid];
     }
 
-    // ---- epilogue: bias, ReLU, NCHW store (lanes = consecutive pixels)
+    // ---- epilogue: bias, ReLU, NCHW store (lanes = consecutive pixels).  The
+    // FN pixel blocks of one output channel are stored one after the other,
+    // so that a channel's run of FN * 32 pixels reaches L2 in consecutive
+    // instructions (with the blocks stored far apart, 128 x 128 tiles on
+    // planes that are not a whole number of cache lines wrote 1.36x their
+    // output to HBM: partial lines written back separately).
+    float* yb[FN];
+    bool mok[FN];
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
         const int mc = m0 + wn * FN * 32 + j * 32 + l32;
-        if (mc >= p.M) continue;
-        const int n = mc / p.PQ;
-        const int pq = mc - n * p.PQ;
-        float* yb = p.y + n * p.K * p.PQ + pq;
+        mok[j] = mc < p.M;
+        const int n = mok[j] ? mc / p.PQ : 0;
+        const int pq = mok[j] ? mc - n * p.PQ : 0;
+        yb[j] = p.y + n * p.K * p.PQ + pq;
+    }
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
+    for (int i = 0; i < FM; ++i) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int kr = k0 + wm * FM * 32 + i * 32 + 8 * (v / 4) + 4 * half + (v % 4);
-                if (kr < p.Kg) {
-                    const int ko = g * p.Kg + kr;
-                    float val = acc[i][j][v];
-                    if (p.splits > 1) {
-                        atomicAdd(yb + ko * p.PQ, val);
-                    } else {
-                        if (p.bias) val += p.bias[ko];
-                        if (p.relu) val = val > 0.0f ? val : 0.0f;
-                        yb[ko * p.PQ] = val;
-                    }
+        for (int v = 0; v < 16; ++v) {
+            const int kr = k0 + wm * FM * 32 + i * 32 + 8 * (v / 4) + 4 * half + (v % 4);
+            if (kr >= p.Kg) continue;
+            const int ko = g * p.Kg + kr;
+            const float bv = (p.splits == 1 && p.bias) ? p.bias[ko] : 0.0f;
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                if (!mok[j]) continue;
+                float val = acc[i][j][v];
+                if (p.splits > 1) {
+                    atomicAdd(yb[j] + ko * p.PQ, val);
+                } else {
+                    if (p.bias) val += bv;
+                    if (p.relu) val = val > 0.0f ? val : 0.0f;
+                    yb[j][ko * p.PQ] = val;
                 }
             }
         }
