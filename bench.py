@@ -80,14 +80,20 @@ HOST_ONLY_SOURCES = ("api.hip", "tuner.hip", "netfile.cpp")
 
 
 def source_digest():
-    """Digest of the kernel sources (and their launchers) under csrc/."""
+    """Digest of the kernel sources (and their launchers) under csrc/, without
+    their comments and blank lines (a comment edit changes no kernel)."""
+    import re
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1511_07376_amd", "csrc")
     for f in sorted(os.listdir(csrc)):
         if f in HOST_ONLY_SOURCES:
             continue
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + fh.read())
+        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        code = "\n".join(l.rstrip() for l in text.splitlines() if l.strip())
+        h.update(f.encode() + code.encode())
     return h.hexdigest()[:16]
 
 
@@ -173,13 +179,17 @@ def cpu_baseline(net, x, params, budget_s, y_gpu=None):
 
 
 def conv_sweep(args):
-    """Single-layer conv sweep: each case auto-tunes on its first call, then
-    `--steps` launches are timed between two HIP events on the launch stream."""
+    """Single-layer conv sweep: each case auto-tunes on its first call (unless
+    --no-autotune; --tuning-file imports recorded choices), then `--steps`
+    launches are timed between two HIP events on the launch stream."""
     import torch
     from paper_1511_07376_amd import cnn
     from paper_1511_07376_amd import workloads as wl
 
-    cnn.cnn_set_autotune(True)
+    if args.tuning_file and os.path.exists(args.tuning_file):
+        with open(args.tuning_file) as f:
+            cnn.cnn_tuning_import(f.read())
+    cnn.cnn_set_autotune(args.autotune)
     for shape in wl.SWEEP_SHAPES:
         c, h, w_, k, r, s_, stride, pad = shape
         for n in wl.SWEEP_BATCHES:
@@ -212,6 +222,9 @@ def conv_sweep(args):
                 rec["miopen_us"] = round(ms_m * 1e3, 2)
             print(json.dumps(rec), flush=True)
     cnn.cnn_set_autotune(False)
+    if args.save_tuning:
+        with open(args.save_tuning, "w") as f:
+            f.write(cnn.cnn_tuning_export())
 
 
 def conv_shapes(net, batch, cnn):
@@ -325,6 +338,63 @@ def single_layer(args):
     print(json.dumps(rec), flush=True)
 
 
+# Shapes on which the built-in tile heuristic was fitted: AlexNet's five
+# conv layers as the network runs them (conv2 and conv3 on bordered input),
+# the conv sweep's five shapes, and the conv layers of LeNet and CIFAR-10
+# quick past their first; (C, H, W, K, R, stride, pad, groups).
+CONFIG_TABLE_SHAPES = [
+    (3, 227, 227, 96, 11, 4, 0, 1), (96, 31, 31, 256, 5, 1, 0, 2), (256, 15, 15, 384, 3, 1, 0, 1),
+    (384, 13, 13, 384, 3, 1, 1, 2), (384, 13, 13, 256, 3, 1, 1, 2),
+    (3, 224, 224, 64, 7, 2, 3, 1), (64, 56, 56, 64, 3, 1, 1, 1), (256, 28, 28, 256, 3, 1, 1, 1),
+    (512, 14, 14, 512, 3, 1, 1, 1), (256, 56, 56, 64, 1, 1, 0, 1),
+    (20, 12, 12, 50, 5, 1, 0, 1), (32, 16, 16, 32, 5, 1, 2, 1), (32, 8, 8, 64, 5, 1, 2, 1),
+]
+
+
+def config_table(args):
+    """Every conv tile configuration, and the built-in heuristic (config -1),
+    timed on CONFIG_TABLE_SHAPES at batches 1, 16, 64 and 256 (256 only where
+    the input holds at most 100k elements per image): 2 warm-up launches, then
+    the mean of 10 between HIP events.  One JSON line per shape, then one
+    line with the heuristic's total against always taking the fastest."""
+    import torch
+    from paper_1511_07376_amd import cnn
+
+    gen = torch.Generator(device="cuda").manual_seed(args.seed)
+    tot_h = tot_best = 0.0
+    ncfg = cnn.cnn_conv2d_num_configs()
+    for n in (1, 16, 64, 256):
+        for (c, h, w_, k, r, st, pd, g) in CONFIG_TABLE_SHAPES:
+            if n == 256 and h * w_ * c > 100000:
+                continue
+            x = torch.rand((n, c, h, w_), device="cuda", generator=gen)
+            wt = torch.randn((k, c // g, r, r), device="cuda", generator=gen) * 0.05
+            b = torch.randn(k, device="cuda", generator=gen)
+            p_, q_ = cnn.cnn_conv2d_out_shape(h, w_, r, r, st, pd)
+            y = torch.empty((n, k, p_, q_), device="cuda")
+            us = {}
+            for cfg in range(-1, ncfg):
+                for _ in range(2):
+                    cnn.cnn_conv2d_fwd(x, wt, b, st, pd, g, True, y=y, config=cfg)
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(10):
+                    cnn.cnn_conv2d_fwd(x, wt, b, st, pd, g, True, y=y, config=cfg)
+                e1.record()
+                torch.cuda.synchronize()
+                us[cfg] = round(e0.elapsed_time(e1) / 10 * 1000, 2)
+            best = min((v, cfg) for cfg, v in us.items() if cfg >= 0)
+            tot_h += us[-1]
+            tot_best += best[0]
+            print(json.dumps({"shape": {"N": n, "C": c, "H": h, "W": w_, "K": k, "R": r, "stride": st, "pad": pd,
+                                        "groups": g}, "us": {str(cf): v for cf, v in us.items()},
+                              "best_config": best[1], "heuristic_over_best": round(us[-1] / best[0], 4)}), flush=True)
+            del x, y
+    print(json.dumps({"heuristic_total_us": round(tot_h, 1), "best_total_us": round(tot_best, 1),
+                      "heuristic_over_best": round(tot_h / tot_best, 4)}), flush=True)
+
+
 def gemm_reference(args):
     """Each conv layer of the network beside torch's fp32 batched GEMM on the
     same contraction with the im2col matrix already unrolled in memory (so the
@@ -419,6 +489,9 @@ def main():
     ap.add_argument("--flush-mb", type=int, default=0, metavar="MIB",
                     help="read a buffer of MIB MiB before each timed call (--single-layer) or before each "
                          "step of the per-layer event pass, so that caches start cold")
+    ap.add_argument("--config-table", action="store_true",
+                    help="instead of the network: time every conv tile configuration and the built-in heuristic "
+                         "on the shapes the heuristic was fitted to, one JSON line per shape")
     ap.add_argument("--gemm-reference", action="store_true",
                     help="instead of the network: time each conv layer beside torch's fp32 batched GEMM "
                          "on its contraction with the im2col matrix precomputed, one JSON line per layer")
@@ -437,6 +510,8 @@ def main():
         return gemm_reference(args)
     if args.single_layer:
         return single_layer(args)
+    if args.config_table:
+        return config_table(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the images of a batch are independent: on N GPUs each would run batch/N)",

@@ -22,10 +22,12 @@ struct ConvConfig {
 const ConvConfig kConfigs[] = {CNN_CONV_CONFIGS(CNN_CONV_ENTRY)};
 constexpr int kNumConfigs = sizeof(kConfigs) / sizeof(kConfigs[0]);
 
-// Heuristic choice when no tuned entry exists, fitted to measured times of
-// every configuration on AlexNet's, LeNet's and CIFAR-10 quick's layers and
-// the single-layer sweep shapes at batches 1 to 256 (its total over those 46
-// shapes is within 1% of always picking the fastest).  t64: output tiles of a
+// Heuristic choice when no tuned entry exists, fitted by hand to measured
+// times of every configuration on AlexNet's, LeNet's and CIFAR-10 quick's
+// layers and the single-layer sweep shapes at batches 1 to 256 (`python
+// bench.py --config-table` times them all: over those 46 shapes the
+// heuristic's total came within 0.5% of always picking the fastest on the
+// box it was fitted on, and 4.2% over on another).  t64: output tiles of a
 // 64 x 64 tile; b128: of a 128 x 128 tile.
 int heuristic_config(const ConvParams& p, int G) {
     const int64_t t64 = (int64_t)ceil_div(p.M, 64) * ceil_div(p.Kg, 64) * G;
