@@ -88,6 +88,27 @@ def test_conv_sweep_batch64_sampled(gpu, shape):
     _conv_case(gpu, 64, C, H, W, K, R, S, st, pd, 1, seed=4, sample=[0, 63])
 
 
+@pytest.mark.parametrize("batch", [16, 64])
+@pytest.mark.parametrize("shape", wl.SWEEP_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_conv_sweep_every_config(gpu, shape, batch):
+    """Every tile configuration on each conv-sweep shape at batches 16 and 64
+    (the benchmark's sweep auto-tunes, so any of them may be the one timed);
+    sampled images."""
+    C, H, W, K, R, S, st, pd = shape
+    x = wl.normal((batch, C, H, W), 1.0, 24, 0)
+    w = wl.normal((K, C, R, S), 1.0, 24, 1)
+    b = wl.normal((K,), 1.0, 24, 2)
+    rows = [0, batch - 1]
+    ref = oracle.conv2d_fwd(x[rows], w, b, (st, st), (pd, pd), 1, True)
+    xd, wd, bd = to_dev(x), to_dev(w), to_dev(b)
+    for cfg in range(gpu.cnn_conv2d_num_configs()):
+        print(f"sweep {shape} N{batch} config {cfg}", flush=True)
+        y = gpu.cnn_conv2d_fwd(xd, wd, bd, st, pd, 1, True, config=cfg)
+        torch.cuda.synchronize()
+        assert_gemm_close(y[rows].cpu().numpy(), ref, C * R * S, f"config {cfg}")
+        del y
+
+
 # The five AlexNet conv layers at batch 64 as the network runs them: conv2
 # and conv3 read planes that the LRN + pooling kernel before them wrote
 # inside a zero border of their padding width, and run unpadded on the
