@@ -438,24 +438,28 @@ conv2d_igemm_f32(ConvParams p) {
             load_x(slab_k(it + j + ST), j);
             load_w(slab_k(it + j + ST), j);
             compute(j & 1);
-            {
+            if constexpr (!STRIDED) {
                 // Instruction order within the slab: the fragment reads, then
                 // the matrix-core instructions with one of the next slabs'
-                // global loads after each (the strided gather: after each of
-                // the second half only), rather than all loads ahead of the
+                // global loads after each, rather than all loads ahead of the
                 // reads.  Measured on AlexNet at batch 64: conv2/conv3 3-5%
-                // and the stride-4 conv1 2-3% faster than the compiler's order;
-                // one load per two instructions, or two per instruction, was
-                // slower.
+                // faster than the compiler's order; one load per two
+                // instructions, or two per instruction, was slower.  The
+                // strided gathers keep the compiler's order: pinned, the
+                // 512-thread tiles returned zeros for the last tap of every
+                // other slab in the last lanes of a wave whenever two
+                // workgroups shared a compute unit (the last gather load of
+                // the slab read a reused address register); the compiler's
+                // order gave exact results, at 3% on the stride-4 stem
+                // (AlexNet conv1 at batch 64: 132 -> 136 us).
                 constexpr int NR = (FM + FN) * (BK / 8);  // fragment reads
                 constexpr int NM = FM * FN * (BK / 2);    // matrix-core instructions
                 constexpr int NL = KRUN + WV;             // global loads
-                constexpr int Q0 = STRIDED ? NM / 2 : 0;  // instructions before the first load
                 __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);  // LDS reads
 #pragma unroll
                 for (int q = 0; q < NM; ++q) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-                    if (q >= Q0 && q - Q0 < NL) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+                    if (q < NL) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
                 }
             }
         }
