@@ -127,6 +127,21 @@ int cnn_fc_fwd(const float* x, int N, int I, const float* w,
                const float* bias, int O, int fuse_relu, float* y,
                cnn_stream_t stream);
 
+/* Number of FC kernel configurations in this build, and a readable name for
+ * configuration i (NULL when out of range). */
+int cnn_fc_num_configs(void);
+const char* cnn_fc_config_name(int i);
+
+/* cnn_fc_fwd (Sec. 3.1) with an explicit kernel configuration: 0 <= config <
+ * cnn_fc_num_configs(), or -1 for the built-in choice.  Every configuration
+ * computes the same function; CNN_ERR_UNSUPPORTED when the configuration
+ * does not take the shape (a batch above its limit, or, for the ones that
+ * load 128 bits at a time, I not a multiple of 4 or x, w not 16-byte
+ * aligned).  Same arguments and ownership as cnn_fc_fwd otherwise. */
+int cnn_fc_fwd_config(const float* x, int N, int I, const float* w,
+                      const float* bias, int O, int fuse_relu, float* y,
+                      int config, cnn_stream_t stream);
+
 typedef enum cnn_pool_mode { CNN_POOL_MAX = 0, CNN_POOL_AVG = 1 } cnn_pool_mode;
 
 /* Max / mean pooling layer (Sec. 3.1).  Window (p, q) covers rows

@@ -90,6 +90,10 @@ lib.cnn_net_graph_destroy.argtypes = [_p]
 lib.cnn_conv2d_num_configs.argtypes = []
 lib.cnn_conv2d_config_name.argtypes = [_i]
 lib.cnn_conv2d_config_name.restype = ctypes.c_char_p
+lib.cnn_fc_fwd_config.argtypes = lib.cnn_fc_fwd.argtypes[:8] + [_i, _p]
+lib.cnn_fc_num_configs.argtypes = []
+lib.cnn_fc_config_name.argtypes = [_i]
+lib.cnn_fc_config_name.restype = ctypes.c_char_p
 lib.cnn_set_autotune.argtypes = [_i]
 lib.cnn_tuning_export.argtypes = [ctypes.c_char_p, ctypes.c_size_t]
 lib.cnn_tuning_export.restype = ctypes.c_size_t
@@ -101,7 +105,7 @@ for _name in ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "c
               "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_softmax_fwd", "cnn_net_out_shape",
               "cnn_net_fwd",
               "cnn_net_fwd_timed", "cnn_net_fwd_dump", "cnn_net_fwd_noalloc", "cnn_conv2d_fwd_config",
-              "cnn_conv2d_num_configs",
+              "cnn_conv2d_num_configs", "cnn_fc_fwd_config", "cnn_fc_num_configs",
               "cnn_set_autotune", "cnn_tuning_import", "cnn_tuning_clear", "cnn_netfile_parse",
               "cnn_net_graph_create", "cnn_net_graph_launch", "cnn_net_graph_destroy"):
     getattr(lib, _name).restype = _i
@@ -111,7 +115,8 @@ EXPORTED = ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn
             "cnn_net_workspace_bytes", "cnn_net_fwd", "cnn_net_fwd_timed", "cnn_net_fwd_dump",
             "cnn_net_fwd_noalloc", "cnn_last_error",
             "cnn_version", "cnn_conv2d_num_configs", "cnn_conv2d_config_name",
-            "cnn_conv2d_fwd_config", "cnn_set_autotune", "cnn_tuning_export",
+            "cnn_conv2d_fwd_config", "cnn_fc_num_configs", "cnn_fc_config_name", "cnn_fc_fwd_config",
+            "cnn_set_autotune", "cnn_tuning_export",
             "cnn_tuning_import", "cnn_tuning_clear", "cnn_netfile_parse", "cnn_net_graph_create",
             "cnn_net_graph_launch", "cnn_net_graph_destroy")
 
@@ -231,16 +236,31 @@ def cnn_tuning_clear() -> None:
     _ok(lib.cnn_tuning_clear())
 
 
-def cnn_fc_fwd(x, w, bias=None, fuse_relu=False, y=None, stream=None):
-    """x [N][I] (or [N][C][H][W], read flattened), w [O][I] -> y [N][O]."""
+def cnn_fc_fwd(x, w, bias=None, fuse_relu=False, y=None, stream=None, config=None):
+    """x [N][I] (or [N][C][H][W], read flattened), w [O][I] -> y [N][O].
+
+    config=None calls cnn_fc_fwd (the built-in kernel choice); an int calls
+    cnn_fc_fwd_config with that configuration (-1: the built-in choice)."""
     N = x.shape[0]
     I = x.numel() // max(N, 1) if N else int(w.shape[1])
     O = w.shape[0]
     if y is None:
         y = torch.empty((N, O), dtype=torch.float32, device=x.device)
-    _ok(lib.cnn_fc_fwd(_dev(x, "x"), N, I, _dev(w, "w"), _dev(bias, "bias"), O, int(fuse_relu),
-                       _dev(y, "y"), _stream(stream)))
+    args = (_dev(x, "x"), N, I, _dev(w, "w"), _dev(bias, "bias"), O, int(fuse_relu), _dev(y, "y"))
+    if config is None:
+        _ok(lib.cnn_fc_fwd(*args, _stream(stream)))
+    else:
+        _ok(lib.cnn_fc_fwd_config(*args, int(config), _stream(stream)))
     return y
+
+
+def cnn_fc_num_configs() -> int:
+    return int(lib.cnn_fc_num_configs())
+
+
+def cnn_fc_config_name(i: int) -> Optional[str]:
+    r = lib.cnn_fc_config_name(int(i))
+    return None if r is None else r.decode()
 
 
 def cnn_pool_fwd(x, mode="max", kernel=2, stride=2, pad=0, ceil_mode=True, fuse_relu=False,

@@ -547,6 +547,19 @@ int cnn_fc_fwd(const float* x, int N, int I, const float* w, const float* bias, 
     return launch_fc(x, N, I, w, bias, O, fuse_relu != 0, y, as_stream(stream));
 }
 
+int cnn_fc_num_configs(void) { return fc_num_configs(); }
+
+const char* cnn_fc_config_name(int i) { return fc_config_name(i); }
+
+int cnn_fc_fwd_config(const float* x, int N, int I, const float* w, const float* bias, int O,
+                      int fuse_relu, float* y, int config, cnn_stream_t stream) {
+    if ((N != 0 && (!x || !y)) || !w) return fail(CNN_ERR_INVALID, "fc: null x, w or y");
+    if (config < -1 || config >= fc_num_configs()) return fail(CNN_ERR_INVALID, "fc: no configuration %d", config);
+    int rc = check_fc(N, I, O);
+    if (rc) return rc;
+    return launch_fc(x, N, I, w, bias, O, fuse_relu != 0, y, as_stream(stream), false, nullptr, false, config);
+}
+
 int cnn_pool_fwd(const float* x, int N, int C, int H, int W, int mode, int kh, int kw, int sh,
                  int sw, int ph, int pw, int ceil_mode, int fuse_relu, float* y, int32_t* idx,
                  cnn_stream_t stream) {

@@ -73,12 +73,17 @@ int conv2d_planned_config(const ConvShape& s, bool no_tune = false);
 // layer's ReLU would need a pass of its own (split reduction), skip it and set
 // *relu_left, so that the caller can fold it into the next layer's input.
 // prefilled: y already holds the bias (see fc_splits, launch_bias_fills).
+// config: an FC kernel configuration (0 <= config < fc_num_configs()), or -1
+// for the built-in choice.
 int launch_fc(const float* x, int N, int I, const float* w, const float* bias, int O, int relu,
               float* y, hipStream_t st, bool relu_in = false, bool* relu_left = nullptr,
-              bool prefilled = false);
-// Reduction splits launch_fc uses for this shape; above 1 its output must
-// start as the bias (launch_fc fills it unless told it is prefilled).
-// Batches of at most kGemvMaxN images take an unsplit matrix-vector kernel.
+              bool prefilled = false, int config = -1);
+int fc_num_configs();
+const char* fc_config_name(int i);
+// Reduction splits of the built-in choice for this shape (launch_fc with
+// config -1); above 1 its output must start as the bias (launch_fc fills it
+// unless told it is prefilled).  Batches of at most kGemvMaxN images take an
+// unsplit matrix-vector kernel.
 constexpr int kGemvMaxN = 2;
 int fc_splits(int N, int I, int O);
 // y_j[n][o][i] = bias_j[o] (or 0), i < inner, for several layer outputs

@@ -239,6 +239,109 @@ __global__ void fc_fill_bias(float* y, const float* bias, int N, int O) {
         y[i] = bias ? bias[i % O] : 0.0f;
 }
 
+// Batches of at most 64 images (NB blocks of 32): each wave owns OB blocks of
+// 32 output features and a run of the reduction, for every image, and feeds
+// the matrix cores straight from its registers: lane (i, h) loads row i of
+// the images' and of the weights' slab as float4s at taps 8q + 4h .. 8q + 4h
+// + 3 of a 32-tap chunk, so its own registers hold the MFMA operands for
+// every k-step (half h is the k index of the instruction) and no LDS stage
+// or barrier sits in the reduction loop.  Two chunks are in flight per wave.
+// The KW waves of a workgroup take consecutive runs of the reduction for the
+// same outputs; their partial tiles are summed through LDS in a fixed order,
+// and a split reduction (grid y > 1) adds the workgroups' sums atomically to
+// an output pre-filled with the bias.  With a small batch the weight tiles
+// are not shared between waves, so nothing is lost by skipping LDS, and the
+// grid can be sized to two waves per SIMD however few output tiles there are
+// (AlexNet's fc8 at batch 64 has 16 tiles of 64 x 64).
+template <int NB, int OB, int KW, bool RELU_X>
+__global__ void __launch_bounds__(64 * KW) fc_direct_f32(FcParams p) {
+    constexpr int Q = 4;            // float4 loads per row and chunk (32 taps)
+    constexpr int TILES = NB * OB;  // 32 x 32 accumulator tiles per wave
+    __shared__ float red[KW * TILES * 16 * 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int i = lane & 31, h = lane >> 5;
+    const int o0 = blockIdx.x * (OB * 32);
+    const int kbase = (blockIdx.y * KW + wave) * p.kchunk;  // this wave's first tap
+    const int kend = min(p.I, kbase + p.kchunk);
+    const int nch = kend > kbase ? (kend - kbase + 31) / 32 : 0;
+    // rows past N (images) or past O (features) lie past the resources' ends
+    const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(p.x), (short)0, p.N * p.I * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(p.w + (size_t)o0 * p.I), (short)0, min(OB * 32, p.O - o0) * p.I * 4, 0x00020000);
+
+    floatx16 acc[TILES];
+#pragma unroll
+    for (int t = 0; t < TILES; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[t][v] = 0.0f;
+    f32x4 xa[2][NB][Q], wb[2][OB][Q];
+    auto load = [&](int c, int s) {
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int k = kbase + c * 32 + 8 * q + 4 * h;
+            const bool ok = k < kend;  // I is a multiple of 4: a float4 is all in or all out
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                xa[s][nb][q] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                    xres, ok ? ((nb * 32 + i) * p.I + k) * 4 : kOutOfRange, 0, 0));
+#pragma unroll
+            for (int ob = 0; ob < OB; ++ob)
+                wb[s][ob][q] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                    wres, ok ? ((ob * 32 + i) * p.I + k) * 4 : kOutOfRange, 0, 0));
+        }
+    };
+    auto compute = [&](int s) {
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) {
+                    float a = xa[s][nb][q][e];
+                    if constexpr (RELU_X) a = a > 0.0f ? a : 0.0f;
+#pragma unroll
+                    for (int ob = 0; ob < OB; ++ob)
+                        acc[nb * OB + ob] =
+                            __builtin_amdgcn_mfma_f32_32x32x2f32(a, wb[s][ob][q][e], acc[nb * OB + ob], 0, 0, 0);
+                }
+    };
+    if (nch > 0) load(0, 0);
+    for (int c = 0; c < nch; c += 2) {
+        load(c + 1, 1);  // past the run: reads zeros, not multiplied
+        compute(0);
+        if (c + 2 < nch) load(c + 2, 0);
+        if (c + 1 < nch) compute(1);
+    }
+
+    // the waves' partial tiles, summed in wave order (lanes on consecutive words)
+#pragma unroll
+    for (int t = 0; t < TILES; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) red[(wave * TILES * 16 + t * 16 + v) * 64 + lane] = acc[t][v];
+    __syncthreads();
+    constexpr int E = TILES * 16 * 64;
+    const bool split = gridDim.y > 1;
+    for (int e = threadIdx.x; e < E; e += 64 * KW) {
+        float sum = red[e];
+#pragma unroll
+        for (int w = 1; w < KW; ++w) sum += red[w * E + e];
+        const int t = e >> 10, v = (e >> 6) & 15, l = e & 63;
+        const int n = (t / OB) * 32 + 8 * (v >> 2) + 4 * (l >> 5) + (v & 3);
+        const int o = o0 + (t % OB) * 32 + (l & 31);
+        if (n < p.N && o < p.O) {
+            float* dst = p.y + (size_t)n * p.O + o;
+            if (split) {
+                atomicAdd(dst, sum);
+            } else {
+                if (p.bias) sum += p.bias[o];
+                if (p.relu) sum = sum > 0.0f ? sum : 0.0f;
+                *dst = sum;
+            }
+        }
+    }
+}
+
 // Batches of at most kGemvMaxN images: a matrix-vector product per image on
 // the vector ALUs, since a 32-row MFMA tile would be mostly empty.  A
 // workgroup owns R consecutive output features (4, or 1 when there are fewer
@@ -356,9 +459,11 @@ struct FcGeom {
     int target;        // workgroups to aim for (two to four per compute unit)
 };
 
-FcGeom fc_geom(int N) {
-    if (N <= 32) return FcGeom{32, 128, 4 * 32, 512};  // launch_fc_cfg<1, 4, 1, 1, 32, 4>
-    return FcGeom{64, 64, 4 * 16, N <= 64 ? 512 : 1024};  // launch_fc_cfg<2, 2, 1, 1, 16, 4>
+// tm: 32 (launch_fc_cfg<1, 4, 1, 1, 32, 4>) or 64 (launch_fc_cfg<2, 2, 1, 1, 16, 4>);
+// target in workgroups for a batch of N.
+FcGeom fc_geom(int tm, int N) {
+    if (tm == 32) return FcGeom{32, 128, 4 * 32, 512};
+    return FcGeom{64, 64, 4 * 16, N <= 64 ? 512 : 1024};
 }
 
 // Splits and the reduction length per split.
@@ -405,11 +510,96 @@ int launch_fc_cfg(const FcParams& prm0, const FcGeom& g, hipStream_t st, bool* r
     return check_launch("fc_gemm_f32");
 }
 
+// Direct kernel: reduction run per wave, so that the grid has about
+// kDirectWaves waves (two per SIMD) whatever the number of output blocks.
+constexpr int kDirectWaves = 2048;
+struct FcDirectGeom {
+    int ob, kw;  // 32-feature blocks per wave, waves per workgroup
+};
+int fc_direct_split(const FcDirectGeom& g, int I, int O, int* kchunk) {
+    const int groups = ceil_div(O, 32 * g.ob);
+    const int per_group = std::max(1, kDirectWaves / groups);      // waves along the reduction
+    *kchunk = std::max(32, ceil_div(ceil_div(I, per_group), 32) * 32);  // whole 32-tap chunks
+    return ceil_div(ceil_div(I, *kchunk), g.kw);
+}
+
+template <int NB, int OB, int KW, bool RELU_X>
+int launch_fc_direct_t(const FcParams& prm0, hipStream_t st, bool* relu_left, bool prefilled) {
+    FcParams prm = prm0;
+    const int splits = fc_direct_split(FcDirectGeom{OB, KW}, prm.I, prm.O, &prm.kchunk);
+    const dim3 grid(ceil_div(prm.O, 32 * OB), splits), block(64 * KW);
+    if (splits > 1 && !prefilled) {
+        const int total = prm.N * prm.O;
+        hipLaunchKernelGGL(fc_fill_bias, dim3(std::min(ceil_div(total, 256), 2048)), dim3(256), 0, st,
+                           prm.y, prm.bias, prm.N, prm.O);
+    }
+    hipLaunchKernelGGL((fc_direct_f32<NB, OB, KW, RELU_X>), grid, block, 0, st, prm);
+    int rc = check_launch("fc_direct_f32");
+    if (rc != CNN_OK || splits == 1 || !prm.relu) return rc;
+    if (relu_left) {  // the caller applies it
+        *relu_left = true;
+        return CNN_OK;
+    }
+    return launch_relu(prm.y, prm.y, (int64_t)prm.N * prm.O, st);
+}
+
+template <int OB, int KW>
+int launch_fc_direct(const FcParams& prm, bool relu_in, hipStream_t st, bool* relu_left, bool prefilled) {
+    if (prm.N <= 32)
+        return relu_in ? launch_fc_direct_t<1, OB, KW, true>(prm, st, relu_left, prefilled)
+                       : launch_fc_direct_t<1, OB, KW, false>(prm, st, relu_left, prefilled);
+    return relu_in ? launch_fc_direct_t<2, OB, KW, true>(prm, st, relu_left, prefilled)
+                   : launch_fc_direct_t<2, OB, KW, false>(prm, st, relu_left, prefilled);
+}
+
+// The configurations (cnn_fc_fwd_config).
+struct FcConfig {
+    const char* name;
+    int max_n;      // largest batch it takes
+    bool need_vec;  // 128-bit loads only (I % 4 == 0, 16-byte aligned x and w)
+};
+const FcConfig kFcConfigs[] = {
+    {"tiled, 64 images x 64 features, 2x2 waves, 16-tap slabs", 1 << 30, false},
+    {"tiled, 32 images x 128 features, 1x4 waves, 32-tap slabs", 1 << 30, false},
+    {"direct, 32 features per wave, 8 waves", 64, true},
+    {"matrix-vector", kGemvMaxN, false},
+};
+constexpr int kNumFcConfigs = sizeof(kFcConfigs) / sizeof(kFcConfigs[0]);
+
+// Built-in choice (vec: 128-bit loads possible), from kernel-trace times of
+// every configuration on AlexNet's fc6-fc8 at batches 16 and 64 (fc6 9216 ->
+// 4096, fc7 4096 -> 4096, fc8 4096 -> 1000).  Batch 16, each layer alone:
+// tiled 32 x 128 29.3, 16.9, 8.4 us, direct 31.5, 15.9, 6.2 us; in the
+// network (input ReLU deferred from the layer before, event times) fc7 took
+// 21.4 us direct against 20.2 tiled and fc8 9.0 against 11.2, so the direct
+// kernel takes the layers with few output features.  Batch 64: tiled 64 x 64
+// 47.0, 24.7, 11.9 us, direct 63.0, 29.7, 12.1 us (the direct kernel reads
+// the images once per 32 features, twice as often as the 64 x 64 tiles, and
+// at batch 64 that traffic, from L2, is what limits it).
+int fc_heuristic(int N, int I, int O, bool vec) {
+    if (N <= kGemvMaxN) return 3;
+    if (N <= 32) return vec && I <= 4096 && O <= 2048 ? 2 : 1;
+    return 0;
+}
+
+int fc_config_splits(int cfg, int N, int I, int O) {
+    int kchunk;
+    switch (cfg) {
+        case 0: return fc_split(fc_geom(64, N), N, I, O, &kchunk);
+        case 1: return fc_split(fc_geom(32, N), N, I, O, &kchunk);
+        case 2: return fc_direct_split(FcDirectGeom{1, 8}, I, O, &kchunk);
+        default: return 1;
+    }
+}
+
 }  // namespace
 
+int fc_num_configs() { return kNumFcConfigs; }
+
+const char* fc_config_name(int i) { return (i >= 0 && i < kNumFcConfigs) ? kFcConfigs[i].name : nullptr; }
+
 int fc_splits(int N, int I, int O) {
-    int kchunk;
-    return N > 0 && N > kGemvMaxN ? fc_split(fc_geom(N), N, I, O, &kchunk) : 1;
+    return N > 0 ? fc_config_splits(fc_heuristic(N, I, O, I % 4 == 0), N, I, O) : 1;
 }
 
 int launch_bias_fills(const BiasFill* jobs, int n, hipStream_t st) {
@@ -431,8 +621,9 @@ int launch_bias_fills(const BiasFill* jobs, int n, hipStream_t st) {
 }
 
 int launch_fc(const float* x, int N, int I, const float* w, const float* bias, int O, int relu,
-              float* y, hipStream_t st, bool relu_in, bool* relu_left, bool prefilled) {
+              float* y, hipStream_t st, bool relu_in, bool* relu_left, bool prefilled, int config) {
     if (relu_left) *relu_left = false;
+    if (config < -1 || config >= kNumFcConfigs) return fail(CNN_ERR_INVALID, "fc: no configuration %d", config);
     if (N == 0) return CNN_OK;
     // buffer offsets within a workgroup's rows are 31-bit
     if ((int64_t)128 * I * 4 >= ((int64_t)1 << 31))
@@ -449,18 +640,28 @@ int launch_fc(const float* x, int N, int I, const float* w, const float* bias, i
     prm.relu = relu;
     const bool vec = (I % 4 == 0) && ((reinterpret_cast<uintptr_t>(x) & 15) == 0) &&
                      ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
-    if (N <= kGemvMaxN) {  // unsplit: the output needs no fill and the ReLU is applied here
-        static_assert(kGemvMaxN == 2, "one instantiation per batch size");
-        return N == 1 ? launch_fc_gemv<1>(prm, vec, relu_in, st) : launch_fc_gemv<2>(prm, vec, relu_in, st);
+    int cfg = config;
+    if (cfg < 0) {
+        cfg = fc_heuristic(N, I, O, vec);
+        if (kFcConfigs[cfg].need_vec && !vec) cfg = N <= 32 ? 1 : 0;
     }
-    const FcGeom g = fc_geom(N);
-#define CNN_FC_CFG(WMW, WNW, FM, FN, BK, D)                                                                  \
-    (vec ? (relu_in ? launch_fc_cfg<WMW, WNW, FM, FN, BK, D, true, true>(prm, g, st, relu_left, prefilled)    \
-                    : launch_fc_cfg<WMW, WNW, FM, FN, BK, D, true, false>(prm, g, st, relu_left, prefilled))  \
-         : (relu_in ? launch_fc_cfg<WMW, WNW, FM, FN, BK, D, false, true>(prm, g, st, relu_left, prefilled)   \
-                    : launch_fc_cfg<WMW, WNW, FM, FN, BK, D, false, false>(prm, g, st, relu_left, prefilled)))
-    if (N <= 32) return CNN_FC_CFG(1, 4, 1, 1, 32, 4);  // 32 images x 128 features (fc_geom)
-    return CNN_FC_CFG(2, 2, 1, 1, 16, 4);               // 64 x 64
+    if (N > kFcConfigs[cfg].max_n)
+        return fail(CNN_ERR_UNSUPPORTED, "fc: configuration %d takes at most %d images", cfg, kFcConfigs[cfg].max_n);
+    if (kFcConfigs[cfg].need_vec && !vec)
+        return fail(CNN_ERR_UNSUPPORTED, "fc: configuration %d needs I %% 4 == 0 and 16-byte aligned x and w", cfg);
+#define CNN_FC_CFG(G, WMW, WNW, FM, FN, BK, D)                                                                     \
+    (vec ? (relu_in ? launch_fc_cfg<WMW, WNW, FM, FN, BK, D, true, true>(prm, G, st, relu_left, prefilled)          \
+                    : launch_fc_cfg<WMW, WNW, FM, FN, BK, D, true, false>(prm, G, st, relu_left, prefilled))        \
+         : (relu_in ? launch_fc_cfg<WMW, WNW, FM, FN, BK, D, false, true>(prm, G, st, relu_left, prefilled)         \
+                    : launch_fc_cfg<WMW, WNW, FM, FN, BK, D, false, false>(prm, G, st, relu_left, prefilled)))
+    switch (cfg) {
+        case 0: return CNN_FC_CFG(fc_geom(64, N), 2, 2, 1, 1, 16, 4);  // 64 x 64
+        case 1: return CNN_FC_CFG(fc_geom(32, N), 1, 4, 1, 1, 32, 4);  // 32 images x 128 features
+        case 2: return launch_fc_direct<1, 8>(prm, relu_in, st, relu_left, prefilled);
+        default:
+            static_assert(kGemvMaxN == 2, "one instantiation per batch size");
+            return N == 1 ? launch_fc_gemv<1>(prm, vec, relu_in, st) : launch_fc_gemv<2>(prm, vec, relu_in, st);
+    }
 #undef CNN_FC_CFG
 }
 

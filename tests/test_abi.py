@@ -259,6 +259,17 @@ def test_tuning_table_text_roundtrip():
     assert cnn.cnn_tuning_export() == ""
 
 
+def test_fc_config_table_and_rejects():
+    """FC configuration names and argument checks: host-only, no launches."""
+    n = cnn.cnn_fc_num_configs()
+    assert n >= 3 and all(cnn.cnn_fc_config_name(i) for i in range(n))
+    assert cnn.cnn_fc_config_name(n) is None and cnn.cnn_fc_config_name(-1) is None
+    assert L.cnn_fc_fwd_config(FAKE, 4, 8, FAKE, 0, 10, 0, FAKE, n, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_fc_fwd_config(FAKE, 4, 8, FAKE, 0, 10, 0, FAKE, -2, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_fc_fwd_config(FAKE, 4, 0, FAKE, 0, 10, 0, FAKE, 0, 0) == cnn.CNN_ERR_INVALID
+    assert L.cnn_fc_fwd_config(0, 4, 8, FAKE, 0, 10, 0, FAKE, 0, 0) == cnn.CNN_ERR_INVALID
+
+
 def test_workspace_holds_bordered_pool_output():
     """A padded conv after LRN + pooling reads the pooled planes inside their
     zero border: the workspace holds two buffers of the bordered size when

@@ -196,9 +196,12 @@ FC_CASES = [
     (256, 9216, 4096, True, [0, 100, 255]), (256, 4096, 4096, True, [1, 254]),
     (1, 37, 3, False, None), (5, 1001, 31, True, None), (33, 129, 129, False, None),
     (65, 260, 7, True, None), (130, 64, 300, False, None), (3, 4, 1, True, None),
-    # k-streaming kernel (batches up to 64, inputs a multiple of 4): 1 to 4 row
-    # blocks of 16, with and without the reduction split over workgroups
+    # batches up to 64 with inputs a multiple of 4, split and unsplit; the
+    # direct kernel's built-in cases (at most 32 images, 4096 inputs and 2048
+    # features): one and two waves' runs of the reduction, a ragged 32-feature
+    # block
     (48, 512, 300, True, None), (20, 3072, 4100, True, [0, 7, 19]), (64, 96, 17, False, None),
+    (16, 4096, 1000, True, None), (7, 64, 33, False, None), (32, 2048, 2000, True, [0, 31]),
     # batches of 1 and 2: the matrix-vector kernel (128-bit and 32-bit loads,
     # 4-row and 1-row workgroups, a ragged last workgroup); 3 and 4 images on
     # the matrix cores next to them
@@ -219,6 +222,44 @@ def test_fc(gpu, case):
     yg = to_host(gpu.cnn_fc_fwd(to_dev(x), to_dev(w), to_dev(b), relu))
     rows = list(range(N)) if sample is None else sample
     assert_gemm_close(yg[rows], oracle.fc_fwd(x[rows], w, b, relu), I, tag)
+
+
+FC_CFG_CASES = [
+    # N, I, O, relu, sampled rows: AlexNet's fc6-fc8 at batches 16 and 64,
+    # ragged batches, features and reductions (multiples of 4 and not), a
+    # reduction shorter than one 32-tap chunk, batches above 64
+    (64, 9216, 4096, True, [0, 31, 32, 63]), (64, 4096, 4096, True, [1, 62]), (64, 4096, 1000, False, None),
+    (16, 9216, 4096, True, [0, 15]), (16, 4096, 1000, False, None),
+    (33, 1000, 33, True, None), (5, 4100, 70, False, None), (64, 12, 5, True, None),
+    (2, 4096, 300, False, None), (1, 36, 1, True, None), (31, 1001, 31, True, None), (70, 256, 64, False, None),
+]
+
+
+@pytest.mark.parametrize("case", FC_CFG_CASES, ids=[f"fc{c[0]}x{c[1]}to{c[2]}" for c in FC_CFG_CASES])
+def test_fc_every_config(gpu, case):
+    """Every FC configuration on the shape; a configuration that does not take
+    it (batch above its limit, a reduction not a multiple of 4 for the
+    128-bit-load ones) must say so with CNN_ERR_UNSUPPORTED."""
+    N, I, O, relu, sample = case
+    x = wl.uniform01((N, I), 17, 0)
+    w = wl.normal((O, I), 0.05, 17, 1)
+    b = wl.normal((O,), 0.01, 17, 2)
+    rows = list(range(N)) if sample is None else sample
+    ref = oracle.fc_fwd(x[rows], w, b, relu)
+    xd, wd, bd = to_dev(x), to_dev(w), to_dev(b)
+    ran = 0
+    for cfg in range(gpu.cnn_fc_num_configs()):
+        tag = f"fc N{N} I{I} O{O} relu{int(relu)} config {cfg} ({gpu.cnn_fc_config_name(cfg)})"
+        print(tag, flush=True)
+        y = torch.full((N, O), float("nan"), device="cuda")
+        rc = gpu.lib.cnn_fc_fwd_config(xd.data_ptr(), N, I, wd.data_ptr(), bd.data_ptr(), O, int(relu),
+                                       y.data_ptr(), cfg, torch.cuda.current_stream().cuda_stream)
+        if rc == gpu.CNN_ERR_UNSUPPORTED:
+            continue
+        assert rc == 0, gpu.cnn_last_error()
+        assert_gemm_close(to_host(y)[rows], ref, I, tag)
+        ran += 1
+    assert ran >= 2
 
 
 @pytest.mark.parametrize("N", [7, 2])
