@@ -308,3 +308,32 @@ def test_padded_conv_after_lrn_pool(gpu, batch, pad, pool):
     y2 = to_host(model(to_dev(x)))
     assert_gemm_close(y2, ref[-1], 24 * P * Q, f"{pool} pad {pad} B{batch}")
     compare_layers(net, params, x, g, written, ref, gi, ref_idx, f"{pool} pad {pad} B{batch}")
+
+
+# Conv chains straight from conv to conv: pads of 1 and 2, unequal row and
+# column pads, a strided and a grouped producer, a ReLU folded into the
+# producer, a 1x1 conv in between.
+CONV_CHAIN_NET = wl.Net(
+    name="conv_chain",
+    input_chw=(6, 15, 17),
+    layers=(
+        wl.conv(6, 16, 3, 2, 1, relu=True),
+        wl.conv(16, 24, 3, 1, 1, groups=2),
+        wl.relu(),
+        wl.conv(24, 20, (3, 5), 1, (1, 2)),
+        wl.conv(20, 8, 1),
+        wl.conv(8, 12, 3, 1, 1, relu=True),
+        wl.conv(12, 12, (1, 3), 1, (0, 1)),
+        wl.fc(12 * 8 * 9, 10),
+    ),
+    weight_std=0.1, bias_std=0.05,
+)
+
+
+@pytest.mark.parametrize("batch", [1, 4, 16])
+def test_conv_chain(gpu, batch):
+    """Batch 1 splits every conv's reduction (outputs prefilled with the bias,
+    ReLUs left to the next conv); 4 and 16 do not split the larger layers."""
+    print(f"net conv_chain batch {batch}", flush=True)
+    x = wl.make_input(CONV_CHAIN_NET, batch, 21)
+    dump_and_compare(gpu, CONV_CHAIN_NET, wl.make_params(CONV_CHAIN_NET, 21), x)
