@@ -395,6 +395,54 @@ def config_table(args):
                       "heuristic_over_best": round(tot_h / tot_best, 4)}), flush=True)
 
 
+FC_TABLE_SHAPES = [  # (I, O): AlexNet's fc6-fc8, LeNet's ip1-ip2, CIFAR-10 quick's ip1-ip2
+    (9216, 4096), (4096, 4096), (4096, 1000), (800, 500), (500, 10), (1024, 64), (64, 10),
+]
+
+
+def fc_config_table(args):
+    """Every FC kernel configuration, and the built-in choice (config -1),
+    timed on FC_TABLE_SHAPES at batches 1, 16, 32, 64 and 256 (configurations
+    that do not take a shape are left out): fuse_relu on, bias, 2 warm-up
+    calls, then the mean of 20 calls between HIP events.  A call whose
+    reduction is split also runs the kernels that set the output to the bias
+    first and apply the ReLU after (inside a network pass the first runs in a
+    pooling kernel and the second in the next layer's reads).  One JSON line
+    per shape."""
+    import torch
+    from paper_1511_07376_amd import cnn
+
+    gen = torch.Generator(device="cuda").manual_seed(args.seed)
+    ncfg = cnn.cnn_fc_num_configs()
+    for n in (1, 16, 32, 64, 256):
+        for (i_, o_) in FC_TABLE_SHAPES:
+            x = torch.rand((n, i_), device="cuda", generator=gen)
+            wt = torch.randn((o_, i_), device="cuda", generator=gen) * 0.02
+            b = torch.randn(o_, device="cuda", generator=gen)
+            y = torch.empty((n, o_), device="cuda")
+            us = {}
+            for cfg in range(-1, ncfg):
+                try:
+                    for _ in range(2):
+                        cnn.cnn_fc_fwd(x, wt, b, True, y=y, config=cfg)
+                except cnn.CnnError:
+                    continue
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(20):
+                    cnn.cnn_fc_fwd(x, wt, b, True, y=y, config=cfg)
+                e1.record()
+                torch.cuda.synchronize()
+                us[cfg] = round(e0.elapsed_time(e1) / 20 * 1000, 2)
+            best = min((v, cfg) for cfg, v in us.items() if cfg >= 0)
+            print(json.dumps({"shape": {"N": n, "I": i_, "O": o_}, "us": {str(cf): v for cf, v in us.items()},
+                              "names": {str(cf): cnn.cnn_fc_config_name(cf) for cf in us if cf >= 0},
+                              "best_config": best[1], "builtin_over_best": round(us[-1] / best[0], 4)}),
+                  flush=True)
+            del x, y, wt
+
+
 def gemm_reference(args):
     """Each conv layer of the network beside torch's fp32 batched GEMM on the
     same contraction with the im2col matrix already unrolled in memory (so the
@@ -489,6 +537,8 @@ def main():
     ap.add_argument("--flush-mb", type=int, default=0, metavar="MIB",
                     help="read a buffer of MIB MiB before each timed call (--single-layer) or before each "
                          "step of the per-layer event pass, so that caches start cold")
+    ap.add_argument("--fc-config-table", action="store_true",
+                    help="time every FC configuration on the networks' FC shapes (one JSON line per shape)")
     ap.add_argument("--config-table", action="store_true",
                     help="instead of the network: time every conv tile configuration and the built-in heuristic "
                          "on the shapes the heuristic was fitted to, one JSON line per shape")
@@ -512,6 +562,8 @@ def main():
         return single_layer(args)
     if args.config_table:
         return config_table(args)
+    if args.fc_config_table:
+        return fc_config_table(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the images of a batch are independent: on N GPUs each would run batch/N)",

@@ -567,18 +567,25 @@ const FcConfig kFcConfigs[] = {
 constexpr int kNumFcConfigs = sizeof(kFcConfigs) / sizeof(kFcConfigs[0]);
 
 // Built-in choice (vec: 128-bit loads possible), from kernel-trace times of
-// every configuration on AlexNet's fc6-fc8 at batches 16 and 64 (fc6 9216 ->
-// 4096, fc7 4096 -> 4096, fc8 4096 -> 1000).  Batch 16, each layer alone:
-// tiled 32 x 128 29.3, 16.9, 8.4 us, direct 31.5, 15.9, 6.2 us; in the
-// network (input ReLU deferred from the layer before, event times) fc7 took
-// 21.4 us direct against 20.2 tiled and fc8 9.0 against 11.2, so the direct
-// kernel takes the layers with few output features.  Batch 64: tiled 64 x 64
-// 47.0, 24.7, 11.9 us, direct 63.0, 29.7, 12.1 us (the direct kernel reads
-// the images once per 32 features, twice as often as the 64 x 64 tiles, and
-// at batch 64 that traffic, from L2, is what limits it).
+// every configuration on the networks' FC shapes at batches 1 to 256 (`python
+// bench.py --fc-config-table`).  Layers with few output features have few
+// output tiles; the tiled kernels then split the reduction many ways (1M
+// atomic partial sums for AlexNet's fc8 at batch 64, about 4 us of its 12) or,
+// with a short reduction, hardly at all (LeNet's 500 -> 10 at batch 64: one
+// workgroup, 13 us), while the direct kernel sizes its grid to two waves per
+// SIMD whatever the number of tiles: at most 32 images it took fc8 (4096 ->
+// 1000) at batch 16 from 8.4 to 6.0 us, and 500 -> 10 at batch 64 from 13.0
+// to 5.4 us.  It reads the images once per 32 features, twice as often as
+// the 64 x 64 tiles, which is what limits it on wide layers at batch 64
+// (fc6 64.0 against 50.0 us).  In the network at batch 16, with the input's
+// ReLU deferred from the layer before, fc7 (4096 -> 4096) took 21.4 us direct
+// against 20.2 tiled.  Above 64 images, layers of at most 1024 features run
+// 3-45% faster on the 32 x 128 tiles (twice the row tiles of 64 x 64).
 int fc_heuristic(int N, int I, int O, bool vec) {
     if (N <= kGemvMaxN) return 3;
-    if (N <= 32) return vec && I <= 4096 && O <= 2048 ? 2 : 1;
+    if (vec && N <= 64 && I <= 4096 && O <= (N <= 32 ? 2048 : 512)) return 2;
+    if (N <= 32) return 1;
+    if (N > 64 && O <= 1024 && I >= 256) return 1;
     return 0;
 }
 
