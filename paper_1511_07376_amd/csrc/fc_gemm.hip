@@ -570,8 +570,8 @@ constexpr int kNumFcConfigs = sizeof(kFcConfigs) / sizeof(kFcConfigs[0]);
 // every configuration on the networks' FC shapes at batches 1 to 256 (`python
 // bench.py --fc-config-table`).  Layers with few output features have few
 // output tiles; the tiled kernels then split the reduction many ways (1M
-// atomic partial sums for AlexNet's fc8 at batch 64, about 4 us of its 12) or,
-// with a short reduction, hardly at all (LeNet's 500 -> 10 at batch 64: one
+// atomic partial sums for AlexNet's fc8 at batch 64) or, with a short
+// reduction, hardly at all (LeNet's 500 -> 10 at batch 64: one
 // workgroup, 13 us), while the direct kernel sizes its grid to two waves per
 // SIMD whatever the number of tiles: at most 32 images it took fc8 (4096 ->
 // 1000) at batch 16 from 8.4 to 6.0 us, and 500 -> 10 at batch 64 from 13.0
