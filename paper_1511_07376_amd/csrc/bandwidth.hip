@@ -106,7 +106,10 @@ __global__ void __launch_bounds__(kThreads) maxpool_f32(PoolParams p) {
     run_fills(p.fills);
 }
 
-// Division by a runtime constant through a multiply-high (exact for n < 2^31).
+// Division by a runtime constant through a multiply-high (exact for n < 2^31):
+// the unsigned method of Granlund and Montgomery, "Division by invariant
+// integers using multiplication" (PLDI 1994), with l = ceil(log2 d) and
+// m = floor(2^32 (2^l - d) / d) + 1, so that n / d = (mulhi(m, n) + n) >> l.
 struct FastDiv {
     unsigned d, m, l;
 };
