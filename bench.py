@@ -7,7 +7,8 @@ parameter loading from its timings, Sec. 4).  Default workload: the
 AlexNet-shaped network at batch 64.
 
 Prints ONE JSON line: images/s (whole job), per-layer times measured with
-HIP events recorded between the layers of every timed step, the convolution
+HIP events that the layers' own kernels record (start of a layer's first
+kernel, end of its last: cnn_net_fwd_kernel_timed) over timed steps, the convolution
 rate as a fraction of the fp32 matrix-core peak, a roofline entry for the
 dominant kernel, and the CPU oracle's rate on a bounded sample of the same
 workload.
@@ -597,8 +598,11 @@ def main():
     if args.save_tuning:
         with open(args.save_tuning, "w") as f:
             f.write(cnn.cnn_tuning_export())
+    # torch creates an event at its first record: record each once
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(nl + 1)] for _ in range(args.steps)]
-    for evs in events:
+    kstart = [[torch.cuda.Event(enable_timing=True) for _ in range(nl)] for _ in range(args.steps)]
+    kstop = [[torch.cuda.Event(enable_timing=True) for _ in range(nl)] for _ in range(args.steps)]
+    for evs in events + kstart + kstop:
         for e in evs:
             e.record()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -647,34 +651,48 @@ def main():
         end.record()
         torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / args.steps
-    # per-layer region: K more steps with HIP events recorded on the launch
-    # stream between the layers (cnn_net_fwd_timed); the event records add a
-    # few microseconds per layer, so this region is not used for `value`
+    # per-layer region: K more steps in which every layer's kernels record
+    # their own start and end times into its pair of events
+    # (cnn_net_fwd_kernel_timed: no packets of their own between the layers);
+    # then K steps with events recorded between the layers
+    # (cnn_net_fwd_timed), whose records add a few microseconds to each
+    # interval.  Neither region is used for `value`.
     flush = torch.ones(args.flush_mb * (1 << 18), device="cuda") if args.flush_mb else None
     torch.cuda.synchronize()
     start.record()
     for k in range(args.steps):
         if flush is not None:
             flush.max()  # cold caches for this step's layers (outside their events)
+        model(xd, y=yd, kernel_events=(kstart[k], kstop[k]))
+    end.record()
+    torch.cuda.synchronize()
+    ms_step_kevents = start.elapsed_time(end) / args.steps
+    assert torch.isfinite(yd).all().item(), "non-finite output"
+    layer_ms = [float(np.mean([kstart[k][i].elapsed_time(kstop[k][i]) for k in range(args.steps)]))
+                for i in range(nl)]
+
+    torch.cuda.synchronize()
+    start.record()
+    for k in range(args.steps):
+        if flush is not None:
+            flush.max()
         model(xd, y=yd, events=events[k])
     end.record()
     torch.cuda.synchronize()
     ms_step_events = start.elapsed_time(end) / args.steps
-    assert torch.isfinite(yd).all().item(), "non-finite output"
-
-    layer_ms = [float(np.mean([events[k][i].elapsed_time(events[k][i + 1]) for k in range(args.steps)]))
-                for i in range(nl)]
+    layer_ms_markers = [float(np.mean([events[k][i].elapsed_time(events[k][i + 1]) for k in range(args.steps)]))
+                        for i in range(nl)]
     step_ms_events = [events[k][0].elapsed_time(events[k][nl]) for k in range(args.steps)]
     work = layer_work(net, batch, cnn)
     layers = []
-    for (name, kind, flops, byts), ms in zip(work, layer_ms):
-        ent = {"layer": name, "ms": round(ms, 5)}
+    for (name, kind, flops, byts), ms, ms_m in zip(work, layer_ms, layer_ms_markers):
+        ent = {"layer": name, "ms": round(ms, 5), "ms_between_markers": round(ms_m, 5)}
         if kind in ("conv", "fc"):
             tf = flops / (ms * 1e-3) / 1e12 if ms > 0 else 0.0
             ent.update({"gflop": round(flops / 1e9, 4), "tflops": round(tf, 2),
                         "frac_fp32_mfma": round(tf / PEAK_FP32_MFMA_TFLOPS, 4)})
         elif kind == "fused":
-            ent["runs_inside_next_layer"] = True  # the interval holds only the event records
+            ent["runs_inside_next_layer"] = True  # no kernel of its own
         else:
             gbs = byts / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
             ent.update({"mbytes": round(byts / 1e6, 2), "gbs": round(gbs, 1),
@@ -719,6 +737,7 @@ def main():
         "conv_gflops": round(conv_tf * 1e3, 1),
         "conv_frac_fp32_mfma_peak": round(conv_tf / PEAK_FP32_MFMA_TFLOPS, 4),
         "conv_ms": round(conv_ms, 5),
+        "ms_per_step_with_kernel_events": round(ms_step_kevents, 4),
         "ms_per_step_with_layer_events": round(ms_step_events, 4),
         "ms_per_step_with_layer_events_median": round(float(np.median(step_ms_events)), 4),
         "layer_events_after_flush_mb": args.flush_mb,

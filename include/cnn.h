@@ -260,6 +260,31 @@ int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x
                       int N, int C, int H, int W, float* y, void* ws,
                       size_t ws_bytes, void* const* events, cnn_stream_t stream);
 
+/* As cnn_net_fwd, and times every layer by its kernels' own timestamps (the
+ * paper times whole networks and the heaviest conv layer separately,
+ * Sec. 4.2): start_events[i] and stop_events[i] (hipEvent_t, created by the
+ * caller, two distinct events per layer, n_layers of each) receive the start
+ * of layer i's first kernel and the end of its last one, so that
+ * hipEventElapsedTime(start_events[i], stop_events[i]) is the layer's
+ * kernel time, with no marker packets between the layers (unlike
+ * cnn_net_fwd_timed, whose event records add a few microseconds to each
+ * interval).
+ *   - A layer that launches no kernel of its own (a RELU run inside its
+ *     predecessor, an LRN run inside the pooling layer after it) gets both
+ *     events recorded back to back: an interval of about zero.
+ *   - The bias fills of split layers count in the interval of the pooling
+ *     layer that performs them; when no pooling layer can, their one launch
+ *     at the start of the pass is in no interval.
+ *   - A conv layer that the auto-tuner times during this pass counts only
+ *     its final launch, not the candidates' runs.
+ *   - Null arrays, or a null or repeated event for a layer, give
+ *     CNN_ERR_INVALID before any work is enqueued. */
+int cnn_net_fwd_kernel_timed(const cnn_layer_desc* layers, int n_layers,
+                             const float* x, int N, int C, int H, int W,
+                             float* y, void* ws, size_t ws_bytes,
+                             void* const* start_events, void* const* stop_events,
+                             cnn_stream_t stream);
+
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): cnn_net_fwd
  * with the library's own static device scratch as the workspace, of

@@ -77,6 +77,8 @@ lib.cnn_net_workspace_bytes.restype = ctypes.c_size_t
 lib.cnn_net_fwd.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t, _p]
 lib.cnn_net_fwd_timed.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
                                   ctypes.POINTER(ctypes.c_void_p), _p]
+lib.cnn_net_fwd_kernel_timed.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
+                                         ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_void_p), _p]
 lib.cnn_net_fwd_dump.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p, ctypes.c_size_t,
                                  ctypes.POINTER(ctypes.c_void_p), _ip, _p]
 lib.cnn_net_fwd_noalloc.argtypes = [_descp, _i, _p, _i, _i, _i, _i, _p, _p]
@@ -104,7 +106,8 @@ lib.cnn_version.restype = ctypes.c_char_p
 for _name in ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
               "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_softmax_fwd", "cnn_net_out_shape",
               "cnn_net_fwd",
-              "cnn_net_fwd_timed", "cnn_net_fwd_dump", "cnn_net_fwd_noalloc", "cnn_conv2d_fwd_config",
+              "cnn_net_fwd_timed", "cnn_net_fwd_kernel_timed", "cnn_net_fwd_dump", "cnn_net_fwd_noalloc",
+              "cnn_conv2d_fwd_config",
               "cnn_conv2d_num_configs", "cnn_fc_fwd_config", "cnn_fc_num_configs",
               "cnn_set_autotune", "cnn_tuning_import", "cnn_tuning_clear", "cnn_netfile_parse",
               "cnn_net_graph_create", "cnn_net_graph_launch", "cnn_net_graph_destroy"):
@@ -112,7 +115,8 @@ for _name in ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "c
 
 EXPORTED = ("cnn_conv2d_out_shape", "cnn_pool_out_shape", "cnn_conv2d_fwd", "cnn_fc_fwd",
             "cnn_pool_fwd", "cnn_lrn_fwd", "cnn_relu_fwd", "cnn_softmax_fwd", "cnn_net_out_shape",
-            "cnn_net_workspace_bytes", "cnn_net_fwd", "cnn_net_fwd_timed", "cnn_net_fwd_dump",
+            "cnn_net_workspace_bytes", "cnn_net_fwd", "cnn_net_fwd_timed", "cnn_net_fwd_kernel_timed",
+            "cnn_net_fwd_dump",
             "cnn_net_fwd_noalloc", "cnn_last_error",
             "cnn_version", "cnn_conv2d_num_configs", "cnn_conv2d_config_name",
             "cnn_conv2d_fwd_config", "cnn_fc_num_configs", "cnn_fc_config_name", "cnn_fc_fwd_config",
@@ -537,11 +541,17 @@ class Network:
                 c, h, w = layer.out_features, 1, 1
 
     def forward(self, x: torch.Tensor, y: Optional[torch.Tensor] = None, stream=None,
-                events: Optional[Sequence] = None) -> torch.Tensor:
-        """cnn_net_fwd (or cnn_net_fwd_timed with one torch.cuda.Event per layer + 1)."""
+                events: Optional[Sequence] = None,
+                kernel_events: Optional[Tuple[Sequence, Sequence]] = None) -> torch.Tensor:
+        """cnn_net_fwd; cnn_net_fwd_timed with `events` (one torch.cuda.Event
+        per layer + 1); cnn_net_fwd_kernel_timed with `kernel_events` = (starts,
+        stops), one event of each per layer, every event already recorded once
+        (torch creates its events lazily)."""
         N, C, H, W = x.shape
         self._prepare(N)
-        graph = self.execution_mode == "graph" and events is None
+        if events is not None and kernel_events is not None:
+            raise ValueError("events and kernel_events are exclusive")
+        graph = self.execution_mode == "graph" and events is None and kernel_events is None
         if y is None:
             if graph:
                 if N not in self._outs:
@@ -563,7 +573,14 @@ class Network:
                 return y
             _ok(lib.cnn_net_graph_launch(g, _stream(stream)))
             return y
-        if events is None:
+        if kernel_events is not None:
+            starts, stops = kernel_events
+            if len(starts) != len(self.descs) or len(stops) != len(self.descs):
+                raise ValueError("need one start and one stop event per layer")
+            arrs = [(ctypes.c_void_p * len(ev))(*[e.cuda_event if hasattr(e, "cuda_event") else int(e) for e in ev])
+                    for ev in (starts, stops)]
+            _ok(lib.cnn_net_fwd_kernel_timed(*args, arrs[0], arrs[1], _stream(stream)))
+        elif events is None:
             _ok(lib.cnn_net_fwd(*args, _stream(stream)))
         else:
             if len(events) != len(self.descs) + 1:

@@ -32,6 +32,11 @@ int check_launch(const char* what) {
     return CNN_OK;
 }
 
+KernelSpan*& current_span() {
+    thread_local KernelSpan* span = nullptr;
+    return span;
+}
+
 // Output extents are computed in 64 bits (a padding near INT_MAX must not
 // wrap) and must fit an int.
 int conv_out(int H, int W, int R, int S, int sh, int sw, int ph, int pw, int* P, int* Q) {
@@ -305,6 +310,40 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
     return CNN_OK;
 }
 
+// The kernel-timestamp span of layer i of a pass (nothing when starts is
+// null): installed from construction to end().  A layer that enqueues no
+// kernel of its own (executed inside another one, or empty) gets both events
+// recorded at end(), an interval of about zero.
+class LayerSpan {
+  public:
+    LayerSpan(void* const* starts, void* const* stops, int i, hipStream_t st) : st_(st) {
+        if (!starts) return;
+        span_.start = reinterpret_cast<hipEvent_t>(starts[i]);
+        span_.stop = reinterpret_cast<hipEvent_t>(stops[i]);
+        current_span() = &span_;
+        active_ = true;
+    }
+    ~LayerSpan() {
+        if (active_) current_span() = nullptr;
+    }
+    LayerSpan(const LayerSpan&) = delete;
+    LayerSpan& operator=(const LayerSpan&) = delete;
+    int end() {
+        if (!active_) return CNN_OK;
+        current_span() = nullptr;
+        active_ = false;
+        if (span_.started) return check_launch("kernel");
+        if (hipEventRecord(span_.start, st_) != hipSuccess || hipEventRecord(span_.stop, st_) != hipSuccess)
+            return check_launch("hipEventRecord");
+        return CNN_OK;
+    }
+
+  private:
+    KernelSpan span_;
+    hipStream_t st_;
+    bool active_ = false;
+};
+
 // dumps (may be null): per layer, a device buffer that receives the layer's
 // output as the layer list defines it (written[i] = 1), or nothing (written[i]
 // = 0) for a RELU layer executed inside its predecessor, whose dump then holds
@@ -313,7 +352,8 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
 // no_tune: never run the auto-tuner in this pass.
 int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H, int W, float* y,
             void* ws, size_t ws_bytes, void* const* events, hipStream_t st,
-            float* const* dumps = nullptr, int* written = nullptr, bool no_tune = false) {
+            float* const* dumps = nullptr, int* written = nullptr, bool no_tune = false,
+            void* const* span_start = nullptr, void* const* span_stop = nullptr) {
     if (N != 0 && (!x || !y)) return fail(CNN_ERR_INVALID, "net: null input or output");
     if (n > 4096) return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n);
     std::vector<Plan> plan((size_t)std::max(n, 0));
@@ -327,6 +367,11 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
         for (int i = 0; events && i <= n; ++i)
             if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), st) != hipSuccess)
                 return check_launch("hipEventRecord");
+        for (int i = 0; span_start && i < n; ++i) {
+            LayerSpan span(span_start, span_stop, i, st);
+            rc = span.end();
+            if (rc) return rc;
+        }
         return CNN_OK;
     }
     const size_t half = align_up((size_t)mx * sizeof(float));
@@ -382,8 +427,13 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
             if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), st) != hipSuccess)
                 return check_launch("hipEventRecord");
         }
+        LayerSpan span(span_start, span_stop, i, st);
         const Plan& p = plan[i];
-        if (p.skipped) continue;
+        if (p.skipped) {
+            rc = span.end();
+            if (rc) return rc;
+            continue;
+        }
         const cnn_layer_desc& d = L[i];
         float* out = (i == last) ? y : buf[next_buf];
         if (p.split && i != last) out = reinterpret_cast<float*>(split_area + p.split_off);
@@ -444,6 +494,8 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
                 break;
         }
         if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
+        rc = span.end();
+        if (rc) return rc;
         if (dumps && dumps[i]) {
             // the stored output without the zero border a pooling layer may give
             // it, and with a ReLU this layer left to the next one
@@ -632,6 +684,17 @@ int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x
                       cnn_stream_t stream) {
     if (!events) return fail(CNN_ERR_INVALID, "net_fwd_timed: null events");
     return run_net(layers, n_layers, x, N, C, H, W, y, ws, ws_bytes, events, as_stream(stream));
+}
+
+int cnn_net_fwd_kernel_timed(const cnn_layer_desc* layers, int n_layers, const float* x, int N, int C,
+                             int H, int W, float* y, void* ws, size_t ws_bytes, void* const* start_events,
+                             void* const* stop_events, cnn_stream_t stream) {
+    if (!start_events || !stop_events) return fail(CNN_ERR_INVALID, "net_fwd_kernel_timed: null events");
+    for (int i = 0; i < n_layers; ++i)
+        if (!start_events[i] || !stop_events[i] || start_events[i] == stop_events[i])
+            return fail(CNN_ERR_INVALID, "net_fwd_kernel_timed: layer %d needs two distinct events", i);
+    return run_net(layers, n_layers, x, N, C, H, W, y, ws, ws_bytes, nullptr, as_stream(stream), nullptr,
+                   nullptr, false, start_events, stop_events);
 }
 
 int cnn_net_fwd_noalloc(const cnn_layer_desc* layers, int n_layers, const float* x, int N, int C, int H,

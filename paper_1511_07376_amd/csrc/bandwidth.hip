@@ -531,7 +531,7 @@ int launch_copy_planes(const float* src, float* dst, int64_t planes, int P, int 
                        bool relu, hipStream_t st) {
     const int64_t total = planes * P * Q;
     if (total == 0) return CNN_OK;
-    hipLaunchKernelGGL(copy_planes_f32, dim3(grid_for(total)), dim3(kThreads), 0, st, src, dst, total, P, Q,
+    enqueue(copy_planes_f32, dim3(grid_for(total)), dim3(kThreads), 0, st, src, dst, total, P, Q,
                        bh, bw, (int)relu);
     return check_launch("copy_planes_f32");
 }
@@ -567,11 +567,11 @@ int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y
 #define CNN_POOL_LAUNCH(M, I)                                                                              \
     do {                                                                                                   \
         if (w33)                                                                                           \
-            hipLaunchKernelGGL((pool_staged_f32<M, I, 3, 3, 2, 2>), g, b, shm, st, p, ppb, nplanes, fpq, fq); \
+            enqueue((pool_staged_f32<M, I, 3, 3, 2, 2>), g, b, shm, st, p, ppb, nplanes, fpq, fq); \
         else if (w22)                                                                                      \
-            hipLaunchKernelGGL((pool_staged_f32<M, I, 2, 2, 2, 2>), g, b, shm, st, p, ppb, nplanes, fpq, fq); \
+            enqueue((pool_staged_f32<M, I, 2, 2, 2, 2>), g, b, shm, st, p, ppb, nplanes, fpq, fq); \
         else                                                                                               \
-            hipLaunchKernelGGL((pool_staged_f32<M, I, 0, 0, 0, 0>), g, b, shm, st, p, ppb, nplanes, fpq, fq); \
+            enqueue((pool_staged_f32<M, I, 0, 0, 0, 0>), g, b, shm, st, p, ppb, nplanes, fpq, fq); \
     } while (0)
         if (mode == CNN_POOL_MAX && idx)
             CNN_POOL_LAUNCH(0, true);
@@ -586,12 +586,12 @@ int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y
     const dim3 grid(grid_for(p.total)), block(kThreads);
     if (mode == CNN_POOL_MAX) {
         if (idx)
-            hipLaunchKernelGGL(maxpool_f32<true>, grid, block, 0, st, p);
+            enqueue(maxpool_f32<true>, grid, block, 0, st, p);
         else
-            hipLaunchKernelGGL(maxpool_f32<false>, grid, block, 0, st, p);
+            enqueue(maxpool_f32<false>, grid, block, 0, st, p);
         return check_launch("maxpool_f32");
     }
-    hipLaunchKernelGGL(avgpool_f32, grid, block, 0, st, p);
+    enqueue(avgpool_f32, grid, block, 0, st, p);
     return check_launch("avgpool_f32");
 }
 
@@ -612,7 +612,7 @@ int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha
     if (size / 2 > 4 || img >= ((int64_t)1 << 29)) {  // wide windows, huge images
         p.nchunk = 1;
         p.total = N * p.HW;
-        hipLaunchKernelGGL(lrn_across_any_f32, dim3(grid_for(p.total)), dim3(kThreads), 0, st, p,
+        enqueue(lrn_across_any_f32, dim3(grid_for(p.total)), dim3(kThreads), 0, st, p,
                            size / 2);
         return check_launch("lrn_across_any_f32");
     }
@@ -627,11 +627,11 @@ int launch_lrn(const float* x, int N, int C, int H, int W, int size, float alpha
         p.total = nb * p.nchunk * p.HW;
         const dim3 grid(grid_for(p.total)), block(kThreads);
         switch (size / 2) {
-            case 0: hipLaunchKernelGGL((lrn_across_f32<0, kChunk>), grid, block, 0, st, p); break;
-            case 1: hipLaunchKernelGGL((lrn_across_f32<1, kChunk>), grid, block, 0, st, p); break;
-            case 2: hipLaunchKernelGGL((lrn_across_f32<2, kChunk>), grid, block, 0, st, p); break;
-            case 3: hipLaunchKernelGGL((lrn_across_f32<3, kChunk>), grid, block, 0, st, p); break;
-            default: hipLaunchKernelGGL((lrn_across_f32<4, kChunk>), grid, block, 0, st, p); break;
+            case 0: enqueue((lrn_across_f32<0, kChunk>), grid, block, 0, st, p); break;
+            case 1: enqueue((lrn_across_f32<1, kChunk>), grid, block, 0, st, p); break;
+            case 2: enqueue((lrn_across_f32<2, kChunk>), grid, block, 0, st, p); break;
+            case 3: enqueue((lrn_across_f32<3, kChunk>), grid, block, 0, st, p); break;
+            default: enqueue((lrn_across_f32<4, kChunk>), grid, block, 0, st, p); break;
         }
         const int rc = check_launch("lrn_across_f32");
         if (rc != CNN_OK) return rc;
@@ -738,11 +738,11 @@ int launch_lrn_pool(const PoolShape& s, int mode, int relu, int size, float alph
 #define CNN_LRN_POOL_CC(H, CC, KW)                                                                   \
     do {                                                                                             \
         if (mode == CNN_POOL_MAX && idx)                                                             \
-            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 0, true, KW>), grid, block, shm, st, p);         \
+            enqueue((lrn_pool_f32<H, CC, 0, true, KW>), grid, block, shm, st, p);         \
         else if (mode == CNN_POOL_MAX)                                                               \
-            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 0, false, KW>), grid, block, shm, st, p);        \
+            enqueue((lrn_pool_f32<H, CC, 0, false, KW>), grid, block, shm, st, p);        \
         else                                                                                         \
-            hipLaunchKernelGGL((lrn_pool_f32<H, CC, 1, false, KW>), grid, block, shm, st, p);        \
+            enqueue((lrn_pool_f32<H, CC, 1, false, KW>), grid, block, shm, st, p);        \
     } while (0)
 #define CNN_LRN_POOL(H, KW)                  \
     do {                                     \
@@ -774,12 +774,12 @@ int launch_relu(const float* x, float* y, int64_t n, hipStream_t st) {
     int64_t done = 0;
     if (vec && n >= 4) {
         const int64_t n4 = n / 4;
-        hipLaunchKernelGGL(relu_f32x4, dim3(grid_for(n4, 4)), dim3(kThreads), 0, st,
+        enqueue(relu_f32x4, dim3(grid_for(n4, 4)), dim3(kThreads), 0, st,
                            reinterpret_cast<const float4*>(x), reinterpret_cast<float4*>(y), n4);
         done = n4 * 4;
     }
     if (done < n)
-        hipLaunchKernelGGL(relu_f32, dim3(grid_for(n - done)), dim3(kThreads), 0, st, x + done,
+        enqueue(relu_f32, dim3(grid_for(n - done)), dim3(kThreads), 0, st, x + done,
                            y + done, n - done);
     return check_launch("relu_f32");
 }

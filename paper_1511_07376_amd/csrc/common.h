@@ -1,6 +1,7 @@
 // Internal declarations shared by the libcnn translation units.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstddef>
@@ -16,6 +17,41 @@ int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)))
 int check_launch(const char* what);
 
 inline hipStream_t as_stream(cnn_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
+
+// Timing of a layer by its kernels' own timestamps.  While a span is installed
+// on the calling thread, the first kernel the library enqueues gives `start`
+// that kernel's start time and every kernel gives `stop` its end time (the
+// last one's stands), so stop - start covers the layer's kernels and nothing
+// else: no marker packet of its own enters the stream.
+struct KernelSpan {
+    hipEvent_t start = nullptr, stop = nullptr;
+    bool started = false;
+};
+KernelSpan*& current_span();
+
+// Every kernel of the library is enqueued through this.
+template <typename F, typename... Args>
+inline void enqueue(F kernel, const dim3& grid, const dim3& block, uint32_t shm, hipStream_t st, Args... args) {
+    KernelSpan* s = current_span();
+    if (!s) {
+        hipLaunchKernelGGL(kernel, grid, block, shm, st, args...);
+        return;
+    }
+    hipExtLaunchKernelGGL(kernel, grid, block, shm, st, s->started ? nullptr : s->start, s->stop, 0u, args...);
+    s->started = true;
+}
+
+// No span is installed during its lifetime (the auto-tuner's timing runs).
+class SpanPause {
+  public:
+    SpanPause() : saved_(current_span()) { current_span() = nullptr; }
+    ~SpanPause() { current_span() = saved_; }
+    SpanPause(const SpanPause&) = delete;
+    SpanPause& operator=(const SpanPause&) = delete;
+
+  private:
+    KernelSpan* saved_;
+};
 
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }

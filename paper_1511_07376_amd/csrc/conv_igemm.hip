@@ -139,7 +139,7 @@ int launch_conv2d(const ConvShape& s, const float* x, const float* w, const floa
     const int64_t img = (int64_t)s.C * prm.HW;
     const int64_t total = (int64_t)s.N * s.K * prm.PQ;
     if (prm.splits > 1 && !(opt && opt->prefilled)) {
-        hipLaunchKernelGGL(conv::conv_fill_bias, dim3((unsigned)std::min<int64_t>(ceil_div64(total, 256), 4096)),
+        enqueue(conv::conv_fill_bias, dim3((unsigned)std::min<int64_t>(ceil_div64(total, 256), 4096)),
                            dim3(256), 0, st, y, bias, s.K, prm.PQ, total);
         rc = check_launch("conv_fill_bias");
         if (rc != CNN_OK) return rc;

@@ -545,7 +545,7 @@ typedef int (*LaunchFn)(const ConvParams&, bool vec_w, hipStream_t st);
 
 template <int WMW, int WNW, int FM, int FN, int BK, int KS, int ST, bool VEC_W, int GATHER>
 inline void launch_kernel(const ConvParams& prm, dim3 grid, dim3 block, size_t shm, hipStream_t st) {
-    hipLaunchKernelGGL((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, VEC_W, GATHER, KS, ST>), grid, block, shm, st, prm);
+    enqueue((conv2d_igemm_f32<WMW, WNW, FM, FN, BK, VEC_W, GATHER, KS, ST>), grid, block, shm, st, prm);
 }
 
 // Picks the gather mode for the shape and launches one configuration.

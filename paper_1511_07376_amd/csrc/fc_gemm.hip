@@ -434,11 +434,11 @@ template <int N, int R>
 int launch_fc_gemv_r(const FcParams& prm, bool vec, bool relu_in, hipStream_t st) {
     const dim3 grid(ceil_div(prm.O, R)), block(256);
     if (vec) {
-        if (relu_in) hipLaunchKernelGGL((fc_gemv_f32<N, R, true, true>), grid, block, 0, st, prm);
-        else hipLaunchKernelGGL((fc_gemv_f32<N, R, true, false>), grid, block, 0, st, prm);
+        if (relu_in) enqueue((fc_gemv_f32<N, R, true, true>), grid, block, 0, st, prm);
+        else enqueue((fc_gemv_f32<N, R, true, false>), grid, block, 0, st, prm);
     } else {
-        if (relu_in) hipLaunchKernelGGL((fc_gemv_f32<N, R, false, true>), grid, block, 0, st, prm);
-        else hipLaunchKernelGGL((fc_gemv_f32<N, R, false, false>), grid, block, 0, st, prm);
+        if (relu_in) enqueue((fc_gemv_f32<N, R, false, true>), grid, block, 0, st, prm);
+        else enqueue((fc_gemv_f32<N, R, false, false>), grid, block, 0, st, prm);
     }
     return check_launch("fc_gemv_f32");
 }
@@ -494,9 +494,9 @@ int launch_fc_cfg(const FcParams& prm0, const FcGeom& g, hipStream_t st, bool* r
     if (splits > 1) {
         const int total = prm.N * prm.O;
         if (!prefilled)
-            hipLaunchKernelGGL(fc_fill_bias, dim3(std::min(ceil_div(total, 256), 2048)), dim3(256), 0, st,
+            enqueue(fc_fill_bias, dim3(std::min(ceil_div(total, 256), 2048)), dim3(256), 0, st,
                                prm.y, prm.bias, prm.N, prm.O);
-        hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, true, RELU_X>), grid, block, 0, st, prm);
+        enqueue((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, true, RELU_X>), grid, block, 0, st, prm);
         int rc = check_launch("fc_gemm_f32");
         if (rc != CNN_OK) return rc;
         if (prm.relu && relu_left) {  // the caller applies it
@@ -506,7 +506,7 @@ int launch_fc_cfg(const FcParams& prm0, const FcGeom& g, hipStream_t st, bool* r
         if (prm.relu) return launch_relu(prm.y, prm.y, (int64_t)prm.N * prm.O, st);
         return CNN_OK;
     }
-    hipLaunchKernelGGL((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, false, RELU_X>), grid, block, 0, st, prm);
+    enqueue((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, false, RELU_X>), grid, block, 0, st, prm);
     return check_launch("fc_gemm_f32");
 }
 
@@ -530,10 +530,10 @@ int launch_fc_direct_t(const FcParams& prm0, hipStream_t st, bool* relu_left, bo
     const dim3 grid(ceil_div(prm.O, 32 * OB), splits), block(64 * KW);
     if (splits > 1 && !prefilled) {
         const int total = prm.N * prm.O;
-        hipLaunchKernelGGL(fc_fill_bias, dim3(std::min(ceil_div(total, 256), 2048)), dim3(256), 0, st,
+        enqueue(fc_fill_bias, dim3(std::min(ceil_div(total, 256), 2048)), dim3(256), 0, st,
                            prm.y, prm.bias, prm.N, prm.O);
     }
-    hipLaunchKernelGGL((fc_direct_f32<NB, OB, KW, RELU_X>), grid, block, 0, st, prm);
+    enqueue((fc_direct_f32<NB, OB, KW, RELU_X>), grid, block, 0, st, prm);
     int rc = check_launch("fc_direct_f32");
     if (rc != CNN_OK || splits == 1 || !prm.relu) return rc;
     if (relu_left) {  // the caller applies it
@@ -619,7 +619,7 @@ int launch_bias_fills(const BiasFill* jobs, int n, hipStream_t st) {
             most = std::max(most, (int64_t)f.job[j].N * f.job[j].O * f.job[j].inner);
         }
         if (most == 0) continue;
-        hipLaunchKernelGGL(bias_fill_multi, dim3((unsigned)std::min<int64_t>(ceil_div64(most, 256), 2048)),
+        enqueue(bias_fill_multi, dim3((unsigned)std::min<int64_t>(ceil_div64(most, 256), 2048)),
                            dim3(256), 0, st, f);
         const int rc = check_launch("bias_fill_multi");
         if (rc != CNN_OK) return rc;

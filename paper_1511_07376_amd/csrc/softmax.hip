@@ -67,10 +67,10 @@ __global__ void __launch_bounds__(kThreads) softmax_cols_f32(const float* x, flo
 int launch_softmax(const float* x, int N, int C, int HW, float* y, hipStream_t st) {
     if (N == 0) return CNN_OK;
     if (HW == 1) {
-        hipLaunchKernelGGL(softmax_rows_f32, dim3(ceil_div(N, kWaves)), dim3(kThreads), 0, st, x, y, N, C);
+        enqueue(softmax_rows_f32, dim3(ceil_div(N, kWaves)), dim3(kThreads), 0, st, x, y, N, C);
     } else {
         const int64_t cols = (int64_t)N * HW;
-        hipLaunchKernelGGL(softmax_cols_f32, dim3((unsigned)ceil_div64(cols, kThreads)), dim3(kThreads), 0, st,
+        enqueue(softmax_cols_f32, dim3((unsigned)ceil_div64(cols, kThreads)), dim3(kThreads), 0, st,
                            x, y, N, C, HW);
     }
     return check_launch("softmax_f32");

@@ -110,7 +110,10 @@ int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const fl
         autotune = g_autotune != 0;
     }
     if (cfg < 0 && autotune && s.N > 0 && !(opt && opt->no_tune)) {
-        cfg = tune(s, x, w, bias, relu, y, st);
+        {
+            SpanPause pause;  // the candidates' runs are not the layer's
+            cfg = tune(s, x, w, bias, relu, y, st);
+        }
         if (cfg >= 0) {
             std::lock_guard<std::mutex> lock(g_mu);
             g_table[key_of(s)] = cfg;

@@ -225,6 +225,20 @@ def test_net_rejects_before_launch():
     assert L.cnn_net_fwd(descs, 0, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, 0) == cnn.CNN_ERR_INVALID
     assert L.cnn_net_fwd(descs, n, FAKE, 2, 4, H, W, FAKE, FAKE, 1 << 40, 0) == cnn.CNN_ERR_INVALID
     assert L.cnn_net_fwd_timed(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, None, 0) == cnn.CNN_ERR_INVALID
+    # kernel-timestamp spans: both arrays, two distinct non-null events per layer
+    evs = (ctypes.c_void_p * n)(*[FAKE + 16 * i for i in range(n)])
+    evs2 = (ctypes.c_void_p * n)(*[FAKE + 16 * (n + i) for i in range(n)])
+    assert L.cnn_net_fwd_kernel_timed(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, None, evs2, 0) == \
+        cnn.CNN_ERR_INVALID
+    assert L.cnn_net_fwd_kernel_timed(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, evs, None, 0) == \
+        cnn.CNN_ERR_INVALID
+    assert L.cnn_net_fwd_kernel_timed(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, evs, evs, 0) == \
+        cnn.CNN_ERR_INVALID
+    assert "two distinct events" in cnn.cnn_last_error()
+    evs2[3] = None
+    assert L.cnn_net_fwd_kernel_timed(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, evs, evs2, 0) == \
+        cnn.CNN_ERR_INVALID
+    assert "layer 3" in cnn.cnn_last_error()
     assert L.cnn_net_fwd_dump(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, None, None, 0) == \
         cnn.CNN_ERR_INVALID
     assert "dump" in cnn.cnn_last_error()

@@ -97,6 +97,70 @@ def test_timed_forward_matches_and_orders_events(gpu):
     assert_gemm_close(y1, y0, 64, "timed vs untimed")
 
 
+def kernel_timed_pass(model, xd, nl):
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(nl)]
+    stops = [torch.cuda.Event(enable_timing=True) for _ in range(nl)]
+    for e in starts + stops:
+        e.record()   # creates the event
+    y = model(xd, kernel_events=(starts, stops))
+    torch.cuda.synchronize()
+    return y, starts, stops
+
+
+@pytest.mark.parametrize("name,batch", [("cifar_quick", 32), ("alexnet", 16)])
+def test_kernel_timed_forward_matches_and_orders_spans(gpu, name, batch):
+    """cnn_net_fwd_kernel_timed: the same output as the untimed pass; every
+    layer's span is non-negative and ends before the next layer's begins;
+    a layer executed inside another one has an interval of about zero."""
+    net = wl.NETS[name]
+    print(f"kernel-timed {name} batch {batch}", flush=True)
+    x = wl.make_input(net, batch, 4)
+    model = gpu.Network(net, wl.make_params(net, 4))
+    xd = to_dev(x)
+    y0 = to_host(model(xd))
+    nl = len(net.layers)
+    y1, starts, stops = kernel_timed_pass(model, xd, nl)
+    assert_gemm_close(to_host(y1), y0, 64, "kernel-timed vs untimed")
+    span = [starts[i].elapsed_time(stops[i]) for i in range(nl)]
+    gaps = [stops[i].elapsed_time(starts[i + 1]) for i in range(nl - 1)]
+    assert all(t >= 0 for t in span), span
+    assert all(g >= 0 for g in gaps), gaps
+    for i, layer in enumerate(net.layers):
+        if layer.kind == "conv":
+            assert span[i] > 0, (i, span)
+    folded = [i for i, layer in enumerate(net.layers)
+              if layer.kind == "relu" or (layer.kind == "lrn" and i + 1 < nl and net.layers[i + 1].kind == "pool")]
+    for i in folded:
+        assert span[i] < 0.05, (i, span[i])
+    total = starts[0].elapsed_time(stops[nl - 1])
+    assert sum(span) <= total + 1e-3
+
+
+def test_kernel_timed_span_leaves_out_autotuning(gpu):
+    """A conv layer tuned during a kernel-timed pass counts only its final
+    launch: its span is of the order of the same layer's span once tuned, not
+    of the candidates' runs."""
+    net = wl.lenet
+    x = wl.make_input(net, 16, 5)
+    model = gpu.Network(net, wl.make_params(net, 5))
+    xd = to_dev(x)
+    nl = len(net.layers)
+    gpu.cnn_tuning_clear()
+    try:
+        gpu.cnn_set_autotune(True)
+        _, s1, e1 = kernel_timed_pass(model, xd, nl)       # tunes both conv shapes
+        y2, s2, e2 = kernel_timed_pass(model, xd, nl)      # tuned
+        gpu.cnn_set_autotune(False)
+        assert len(gpu.cnn_tuning_export().splitlines()) == 2
+    finally:
+        gpu.cnn_set_autotune(False)
+        gpu.cnn_tuning_clear()
+    for i, layer in enumerate(net.layers):
+        if layer.kind == "conv":
+            first, tuned = s1[i].elapsed_time(e1[i]), s2[i].elapsed_time(e2[i])
+            assert 0 < first < 3 * tuned + 0.05, (i, first, tuned)
+
+
 def test_standalone_relu_layer_is_folded(gpu):
     """A RELU layer after conv / pool runs inside that layer; the result is the same
     as the oracle's separate ReLU."""
