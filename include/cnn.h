@@ -271,7 +271,8 @@ int cnn_net_fwd_timed(const cnn_layer_desc* layers, int n_layers, const float* x
  * interval).
  *   - A layer that launches no kernel of its own (a RELU run inside its
  *     predecessor, an LRN run inside the pooling layer after it) gets both
- *     events recorded back to back: an interval of about zero.
+ *     events recorded back to back after the pass's last kernel: an
+ *     interval of about zero, outside every other layer's span.
  *   - The bias fills of split layers count in the interval of the pooling
  *     layer that performs them; when no pooling layer can, their one launch
  *     at the start of the pass is in no interval.

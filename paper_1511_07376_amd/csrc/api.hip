@@ -311,12 +311,15 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
 }
 
 // The kernel-timestamp span of layer i of a pass (nothing when starts is
-// null): installed from construction to end().  A layer that enqueues no
-// kernel of its own (executed inside another one, or empty) gets both events
-// recorded at end(), an interval of about zero.
+// null): installed from construction to end().  end() reports whether the
+// layer enqueued no kernel of its own (executed inside another one, or
+// empty); run_net then records both of its events after the pass's last
+// kernel, an interval of about zero.  (Recorded in place, the two records
+// delayed the start of the next layer's kernel by ~5 us, inside that layer's
+// span.)
 class LayerSpan {
   public:
-    LayerSpan(void* const* starts, void* const* stops, int i, hipStream_t st) : st_(st) {
+    LayerSpan(void* const* starts, void* const* stops, int i) {
         if (!starts) return;
         span_.start = reinterpret_cast<hipEvent_t>(starts[i]);
         span_.stop = reinterpret_cast<hipEvent_t>(stops[i]);
@@ -328,21 +331,28 @@ class LayerSpan {
     }
     LayerSpan(const LayerSpan&) = delete;
     LayerSpan& operator=(const LayerSpan&) = delete;
-    int end() {
+    int end(bool* empty) {
+        *empty = false;
         if (!active_) return CNN_OK;
         current_span() = nullptr;
         active_ = false;
-        if (span_.started) return check_launch("kernel");
-        if (hipEventRecord(span_.start, st_) != hipSuccess || hipEventRecord(span_.stop, st_) != hipSuccess)
-            return check_launch("hipEventRecord");
-        return CNN_OK;
+        *empty = !span_.started;
+        return span_.started ? check_launch("kernel") : CNN_OK;
     }
 
   private:
     KernelSpan span_;
-    hipStream_t st_;
     bool active_ = false;
 };
+
+// Both events of every layer in `layers` (kernel-less layers), back to back.
+int record_empty_spans(const std::vector<int>& layers, void* const* starts, void* const* stops, hipStream_t st) {
+    for (int i : layers)
+        if (hipEventRecord(reinterpret_cast<hipEvent_t>(starts[i]), st) != hipSuccess ||
+            hipEventRecord(reinterpret_cast<hipEvent_t>(stops[i]), st) != hipSuccess)
+            return check_launch("hipEventRecord");
+    return CNN_OK;
+}
 
 // dumps (may be null): per layer, a device buffer that receives the layer's
 // output as the layer list defines it (written[i] = 1), or nothing (written[i]
@@ -367,10 +377,10 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
         for (int i = 0; events && i <= n; ++i)
             if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), st) != hipSuccess)
                 return check_launch("hipEventRecord");
-        for (int i = 0; span_start && i < n; ++i) {
-            LayerSpan span(span_start, span_stop, i, st);
-            rc = span.end();
-            if (rc) return rc;
+        if (span_start) {
+            std::vector<int> all((size_t)std::max(n, 0));
+            for (int i = 0; i < n; ++i) all[(size_t)i] = i;
+            return record_empty_spans(all, span_start, span_stop, st);
         }
         return CNN_OK;
     }
@@ -422,16 +432,19 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
     const float* cur = x;
     int next_buf = 0;
     bool relu_pending = false;  // cur still needs the previous layer's ReLU
+    std::vector<int> empty_spans;  // layers that enqueued no kernel (spans recorded at the end)
     for (int i = 0; i < n; ++i) {
         if (events) {
             if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), st) != hipSuccess)
                 return check_launch("hipEventRecord");
         }
-        LayerSpan span(span_start, span_stop, i, st);
+        LayerSpan span(span_start, span_stop, i);
+        bool empty = false;
         const Plan& p = plan[i];
         if (p.skipped) {
-            rc = span.end();
+            rc = span.end(&empty);
             if (rc) return rc;
+            if (empty) empty_spans.push_back(i);
             continue;
         }
         const cnn_layer_desc& d = L[i];
@@ -494,8 +507,9 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
                 break;
         }
         if (rc) return fail(rc, "net layer %d: %s", i, std::string(cnn_last_error()).c_str());
-        rc = span.end();
+        rc = span.end(&empty);
         if (rc) return rc;
+        if (empty) empty_spans.push_back(i);
         if (dumps && dumps[i]) {
             // the stored output without the zero border a pooling layer may give
             // it, and with a ReLU this layer left to the next one
@@ -511,6 +525,7 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
         if (hipEventRecord(reinterpret_cast<hipEvent_t>(events[n]), st) != hipSuccess)
             return check_launch("hipEventRecord");
     }
+    if (span_start) return record_empty_spans(empty_spans, span_start, span_stop, st);
     return CNN_OK;
 }
 
