@@ -27,7 +27,7 @@ constexpr int kNumConfigs = sizeof(kConfigs) / sizeof(kConfigs[0]);
 // layers and the single-layer sweep shapes at batches 1 to 256 (`python
 // bench.py --config-table` times them all: over those 46 shapes the
 // heuristic's total came within 0.5% of always picking the fastest on the
-// box it was fitted on, and 4.2-4.9% over on others).  t64: output tiles of a
+// box it was fitted on, and 4.0-4.9% over on others).  t64: output tiles of a
 // 64 x 64 tile; b128: of a 128 x 128 tile.
 int heuristic_config(const ConvParams& p, int G) {
     const int64_t t64 = (int64_t)ceil_div(p.M, 64) * ceil_div(p.Kg, 64) * G;
