@@ -98,11 +98,32 @@ def source_digest():
     return h.hexdigest()[:16]
 
 
-def stored_traffic(workload, layer_name):
+def conv_configs_of(tuning_text, layer):
+    """Tile configurations a tuning table (cnn_tuning_export's text) records
+    for a conv layer: its lines with the layer's input and output channels,
+    filter, stride and groups, sorted.  Height, width and padding are left out:
+    in a network a padded layer may run on a zero-bordered input without
+    padding."""
+    st = layer.stride if isinstance(layer.stride, (tuple, list)) else (layer.stride, layer.stride)
+    want = (layer.in_channels, layer.out_channels, layer.kernel[0], layer.kernel[1], st[0], st[1], layer.groups)
+    cfgs = []
+    for line in tuning_text.splitlines():
+        f = line.split()
+        if len(f) != 13:
+            continue
+        v = [int(t) for t in f]
+        if (v[1], v[4], v[5], v[6], v[7], v[8], v[11]) == want:
+            cfgs.append(v[12])
+    return sorted(cfgs)
+
+
+def stored_traffic(workload, layer_name, layer=None, tuning_text=None, path=None):
     """HBM bytes per launch measured by rocprofv3 --pmc (FETCH_SIZE, WRITE_SIZE),
-    kept with the digest of the kernel sources they were taken on; None when the
-    sources have changed since."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    kept with the digest of the kernel sources and the tuning table they were
+    taken with.  None when the sources have changed since, or, for a conv
+    layer (`layer`), when the current tuning table (`tuning_text`) gives it a
+    different tile configuration from the one the counters saw."""
+    path = path or os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -110,7 +131,13 @@ def stored_traffic(workload, layer_name):
     if rec.get("source_digest") != source_digest():
         return None
     lay = rec.get("layers", {}).get(layer_name)
-    return None if lay is None else lay.get("hbm_bytes_per_launch")
+    if lay is None:
+        return None
+    if layer is not None and layer.kind == "conv":
+        then = conv_configs_of("\n".join(rec.get("tuning", [])), layer)
+        if not then or then != conv_configs_of(tuning_text or "", layer):
+            return None
+    return lay.get("hbm_bytes_per_launch")
 
 
 def host_cpu_model():
@@ -714,7 +741,11 @@ def main():
         ach = dbytes / (layer_ms[dom] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(ach / PEAK_HBM_GBS, 4)}
-    roof["traffic"] = stored_traffic(workload, dname)
+    named, counts = {}, {}
+    for layer in net.layers:  # the names layer_work gives
+        counts[layer.kind] = counts.get(layer.kind, 0) + 1
+        named[f"{layer.kind}{counts[layer.kind]}"] = layer
+    roof["traffic"] = stored_traffic(workload, dname, named.get(dname), cnn.cnn_tuning_export())
     roof["layer"] = dname
     roof["launch_ms"] = round(layer_ms[dom], 5)
 
