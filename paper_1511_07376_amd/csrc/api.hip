@@ -314,9 +314,8 @@ int plan_net(const cnn_layer_desc* L, int n, int N, int C, int H, int W, Plan* p
 // null): installed from construction to end().  end() reports whether the
 // layer enqueued no kernel of its own (executed inside another one, or
 // empty); run_net then records both of its events after the pass's last
-// kernel, an interval of about zero.  (Recorded in place, the two records
-// delayed the start of the next layer's kernel by ~5 us, inside that layer's
-// span.)
+// kernel, an interval of about zero, so that no record packet sits between
+// two kernels of the pass.
 class LayerSpan {
   public:
     LayerSpan(void* const* starts, void* const* stops, int i) {
