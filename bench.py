@@ -126,27 +126,34 @@ def conv_configs_of(tuning_text, layer):
     return sorted(cfgs)
 
 
-def stored_traffic(workload, layer_name, layer=None, tuning_text=None, path=None):
+def stored_traffic(workload, layer_name, layer=None, tuning_text=None, prof_dir=None):
     """HBM bytes per launch measured by rocprofv3 --pmc (FETCH_SIZE, WRITE_SIZE),
     kept with the digest of the kernel sources and the tuning table they were
-    taken with.  None when the sources have changed since, or, for a conv
-    layer (`layer`), when the current tuning table (`tuning_text`) gives it a
-    different tile configuration from the one the counters saw."""
-    path = path or os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
-    if not os.path.exists(path):
-        return None
-    with open(path) as f:
-        rec = json.load(f)
-    if rec.get("source_digest") != source_digest():
-        return None
-    lay = rec.get("layers", {}).get(layer_name)
-    if lay is None:
-        return None
-    if layer is not None and layer.kind == "conv":
-        then = conv_configs_of("\n".join(rec.get("tuning", [])), layer)
-        if not then or then != conv_configs_of(tuning_text or "", layer):
-            return None
-    return lay.get("hbm_bytes_per_launch")
+    taken with: traffic_<workload>.json in `prof_dir` (profiles/), then
+    records taken with other tuning tables (traffic_<workload>_*.json).  The
+    first record that applies gives the figure: the sources unchanged since,
+    and, for a conv layer (`layer`), the same tile configuration in its tuning
+    table as in the current one (`tuning_text`).  None when none applies."""
+    prof = prof_dir or os.path.join(ROOT, "profiles")
+    alts = sorted(f for f in os.listdir(prof) if f.startswith(f"traffic_{workload}_") and f.endswith(".json"))
+    paths = [os.path.join(prof, f) for f in [f"traffic_{workload}.json"] + alts]
+    digest = source_digest()
+    for pth in paths:
+        if not os.path.exists(pth):
+            continue
+        with open(pth) as f:
+            rec = json.load(f)
+        if rec.get("source_digest") != digest:
+            continue
+        lay = rec.get("layers", {}).get(layer_name)
+        if lay is None:
+            continue
+        if layer is not None and layer.kind == "conv":
+            then = conv_configs_of("\n".join(rec.get("tuning", [])), layer)
+            if not then or then != conv_configs_of(tuning_text or "", layer):
+                continue
+        return lay.get("hbm_bytes_per_launch")
+    return None
 
 
 def host_cpu_model():

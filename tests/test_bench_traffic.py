@@ -28,28 +28,34 @@ def test_conv_configs_of_matches_channels_filter_stride_groups():
     assert bench.conv_configs_of("", conv1) == []
 
 
-def _record(tmp_path, digest, tuning):
+def _record(d, name, digest, tuning, conv2_bytes=123):
     rec = {"source_digest": digest, "tuning": tuning.splitlines(),
-           "layers": {"conv2": {"hbm_bytes_per_launch": 123}, "pool3": {"hbm_bytes_per_launch": 7}}}
-    path = tmp_path / "traffic.json"
-    path.write_text(json.dumps(rec))
-    return str(path)
+           "layers": {"conv2": {"hbm_bytes_per_launch": conv2_bytes}, "pool3": {"hbm_bytes_per_launch": 7}}}
+    (d / name).write_text(json.dumps(rec))
 
 
 def test_traffic_needs_the_same_sources_and_tiles(tmp_path):
     conv2 = _layers(wl.alexnet, "conv")[1]
     pool3 = _layers(wl.alexnet, "pool")[2]
-    path = _record(tmp_path, bench.source_digest(), TUNE)
-    assert bench.stored_traffic("w", "conv2", conv2, TUNE, path=path) == 123
+    d = str(tmp_path)
+    _record(tmp_path, "traffic_w.json", bench.source_digest(), TUNE)
+    assert bench.stored_traffic("w", "conv2", conv2, TUNE, prof_dir=d) == 123
     # conv2 tuned to another configuration, or not tuned at all (the heuristic's pick)
-    assert bench.stored_traffic("w", "conv2", conv2, TUNE.replace(" 2 0\n", " 2 2\n"), path=path) is None
-    assert bench.stored_traffic("w", "conv2", conv2, "", path=path) is None
+    other = TUNE.replace(" 2 0\n", " 2 2\n")
+    assert bench.stored_traffic("w", "conv2", conv2, other, prof_dir=d) is None
+    assert bench.stored_traffic("w", "conv2", conv2, "", prof_dir=d) is None
     # a pooling layer has no tiles: the sources decide alone
-    assert bench.stored_traffic("w", "pool3", pool3, "", path=path) == 7
-    assert bench.stored_traffic("w", "fc9", None, TUNE, path=path) is None
-    stale = _record(tmp_path, "0" * 16, TUNE)
-    assert bench.stored_traffic("w", "conv2", conv2, TUNE, path=stale) is None
-    assert bench.stored_traffic("w", "pool3", pool3, TUNE, path=stale) is None
+    assert bench.stored_traffic("w", "pool3", pool3, "", prof_dir=d) == 7
+    assert bench.stored_traffic("w", "fc9", None, TUNE, prof_dir=d) is None
+    # a record taken with the other configuration applies to it, not to the first
+    _record(tmp_path, "traffic_w_conv2cfg2.json", bench.source_digest(), other, conv2_bytes=456)
+    assert bench.stored_traffic("w", "conv2", conv2, other, prof_dir=d) == 456
+    assert bench.stored_traffic("w", "conv2", conv2, TUNE, prof_dir=d) == 123
+    # records of other kernel sources never apply
+    _record(tmp_path, "traffic_w.json", "0" * 16, TUNE)
+    _record(tmp_path, "traffic_w_conv2cfg2.json", "0" * 16, other)
+    assert bench.stored_traffic("w", "conv2", conv2, TUNE, prof_dir=d) is None
+    assert bench.stored_traffic("w", "pool3", pool3, TUNE, prof_dir=d) is None
 
 
 def test_committed_records_carry_their_tuning_table():

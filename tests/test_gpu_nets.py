@@ -141,6 +141,18 @@ def test_kernel_timed_forward_matches_and_orders_spans(gpu, name, batch):
     assert sum(span[i] for i in kern) <= total + 1e-3
 
 
+def test_kernel_timed_empty_batch_records_every_span(gpu):
+    """An empty batch launches nothing but still records both events of every
+    layer (intervals of about zero), like the timed pass's other contract."""
+    net = wl.cifar_quick
+    model = gpu.Network(net, wl.make_params(net, 6))
+    x = torch.empty((0,) + tuple(net.input_chw), device="cuda")
+    y, starts, stops = kernel_timed_pass(model, x, len(net.layers))
+    assert y.shape[0] == 0
+    for a, b in zip(starts, stops):
+        assert 0 <= a.elapsed_time(b) < 0.05
+
+
 def test_kernel_timed_span_leaves_out_autotuning(gpu):
     """A conv layer tuned during a kernel-timed pass counts only its final
     launch: its span is of the order of the same layer's span once tuned, not
