@@ -10,7 +10,10 @@
  * sides.
  *
  * Pass: max |gpu - oracle| <= 1e-4 * sqrt(64) and relative L2 <= 1e-4 on the
- * 32 x 10 logits (the FC criterion of the last layer, Kred = 64).
+ * 32 x 10 logits (the FC criterion of the last layer, Kred = 64).  A second
+ * pass through cnn_net_fwd_kernel_timed, with one pair of HIP events per
+ * layer, must give the same logits (within that tolerance: split reductions
+ * may add in another order) and a non-negative kernel time for every layer.
  * Exit status 0 on pass, 1 on a mismatch, 2 on an API or runtime error. */
 #include <math.h>
 #include <stdint.h>
@@ -134,6 +137,34 @@ int main(void) {
     float y_g[N * 10];
     HIP_OK(hipMemcpy(y_g, y_d, sizeof(y_g), hipMemcpyDeviceToHost));
 
+    /* the same pass again, each layer timed by its kernels' own timestamps */
+    hipEvent_t ev_start[NL], ev_stop[NL];
+    void* starts[NL];
+    void* stops[NL];
+    for (int i = 0; i < NL; ++i) {
+        HIP_OK(hipEventCreate(&ev_start[i]));
+        HIP_OK(hipEventCreate(&ev_stop[i]));
+        starts[i] = ev_start[i];
+        stops[i] = ev_stop[i];
+    }
+    float* y2_d = NULL;
+    HIP_OK(hipMalloc((void**)&y2_d, (size_t)N * 10 * sizeof(float)));
+    CNN_OK_(cnn_net_fwd_kernel_timed(L, NL, x_d, N, 3, 32, 32, y2_d, ws, ws_bytes, starts, stops,
+                                     (cnn_stream_t)st));
+    HIP_OK(hipStreamSynchronize(st));
+    float y_t[N * 10];
+    HIP_OK(hipMemcpy(y_t, y2_d, sizeof(y_t), hipMemcpyDeviceToHost));
+    float span_ms[NL];
+    for (int i = 0; i < NL; ++i) {
+        HIP_OK(hipEventElapsedTime(&span_ms[i], ev_start[i], ev_stop[i]));
+        if (!(span_ms[i] >= 0.0f)) {
+            fprintf(stderr, "layer %d: kernel interval %g ms\n", i, span_ms[i]);
+            return 1;
+        }
+    }
+    double timed_diff = 0.0;
+    for (int i = 0; i < N * 10; ++i) timed_diff = fmax(timed_diff, fabs((double)y_t[i] - (double)y_g[i]));
+
     /* the oracle, layer by layer, ReLU as separate steps */
     float* a = (float*)malloc((size_t)N * 32 * 32 * 32 * sizeof(float));
     float* b = (float*)malloc((size_t)N * 32 * 32 * 32 * sizeof(float));
@@ -171,11 +202,14 @@ int main(void) {
     }
     const double rel = den > 0 ? sqrt(num / den) : 0.0;
     const double tol = 1e-4 * sqrt(64.0);
-    printf("cifar_quick_c: %s, N=%d, max abs err %.3e (tol %.3e), rel L2 %.3e\n", cnn_version(), N, max_err,
-           tol, rel);
+    printf("cifar_quick_c: %s, N=%d, max abs err %.3e (tol %.3e), rel L2 %.3e; kernel-timed pass differs by "
+           "%.3e, layer kernel times (us):", cnn_version(), N, max_err, tol, rel, timed_diff);
+    for (int i = 0; i < NL; ++i) printf(" %.1f", 1000.0 * span_ms[i]);
+    printf("\n");
+    for (int i = 0; i < NL; ++i) { hipEventDestroy(ev_start[i]); hipEventDestroy(ev_stop[i]); }
     hipStreamDestroy(st);
-    hipFree(ws); hipFree(y_d); hipFree(x_d);
+    hipFree(ws); hipFree(y_d); hipFree(y2_d); hipFree(x_d);
     for (int i = 0; i < 5; ++i) { hipFree(w_d[i]); hipFree(b_d[i]); free(w_h[i]); free(b_h[i]); }
     free(x_h); free(a); free(b);
-    return (max_err <= tol && rel <= 1e-4) ? 0 : 1;
+    return (max_err <= tol && rel <= 1e-4 && timed_diff <= tol) ? 0 : 1;
 }
