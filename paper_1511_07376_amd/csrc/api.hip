@@ -704,6 +704,7 @@ int cnn_net_fwd_kernel_timed(const cnn_layer_desc* layers, int n_layers, const f
                              int H, int W, float* y, void* ws, size_t ws_bytes, void* const* start_events,
                              void* const* stop_events, cnn_stream_t stream) {
     if (!start_events || !stop_events) return fail(CNN_ERR_INVALID, "net_fwd_kernel_timed: null events");
+    if (n_layers > 4096) return fail(CNN_ERR_UNSUPPORTED, "net: %d layers", n_layers);  // as run_net, before reading
     for (int i = 0; i < n_layers; ++i)
         if (!start_events[i] || !stop_events[i] || start_events[i] == stop_events[i])
             return fail(CNN_ERR_INVALID, "net_fwd_kernel_timed: layer %d needs two distinct events", i);

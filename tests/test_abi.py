@@ -239,6 +239,8 @@ def test_net_rejects_before_launch():
     assert L.cnn_net_fwd_kernel_timed(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, evs, evs2, 0) == \
         cnn.CNN_ERR_INVALID
     assert "layer 3" in cnn.cnn_last_error()
+    assert L.cnn_net_fwd_kernel_timed(descs, 5000, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, evs, evs2, 0) == \
+        cnn.CNN_ERR_UNSUPPORTED
     assert L.cnn_net_fwd_dump(descs, n, FAKE, 2, C, H, W, FAKE, FAKE, 1 << 40, None, None, 0) == \
         cnn.CNN_ERR_INVALID
     assert "dump" in cnn.cnn_last_error()
