@@ -244,7 +244,8 @@ size_t cnn_net_workspace_bytes(const cnn_layer_desc* layers, int n_layers,
  * output never goes to memory; the values equal those of the two layers run
  * separately, bit for bit); other RELU layers and SOFTMAX layers run in
  * place.  A SOFTMAX layer uses
- * only the type field.  Every layer is validated before the first launch. */
+ * only the type field.  Every layer is validated before the first launch;
+ * a list of more than 4096 layers gives CNN_ERR_UNSUPPORTED. */
 int cnn_net_fwd(const cnn_layer_desc* layers, int n_layers, const float* x,
                 int N, int C, int H, int W, float* y, void* ws, size_t ws_bytes,
                 cnn_stream_t stream);
