@@ -135,6 +135,8 @@ def stored_traffic(workload, layer_name, layer=None, tuning_text=None, prof_dir=
     and, for a conv layer (`layer`), the same tile configuration in its tuning
     table as in the current one (`tuning_text`).  None when none applies."""
     prof = prof_dir or os.path.join(ROOT, "profiles")
+    if not os.path.isdir(prof):
+        return None
     alts = sorted(f for f in os.listdir(prof) if f.startswith(f"traffic_{workload}_") and f.endswith(".json"))
     paths = [os.path.join(prof, f) for f in [f"traffic_{workload}.json"] + alts]
     digest = source_digest()

@@ -58,6 +58,12 @@ def test_traffic_needs_the_same_sources_and_tiles(tmp_path):
     assert bench.stored_traffic("w", "pool3", pool3, TUNE, prof_dir=d) is None
 
 
+def test_no_records_at_all(tmp_path):
+    conv2 = _layers(wl.alexnet, "conv")[1]
+    assert bench.stored_traffic("w", "conv2", conv2, TUNE, prof_dir=str(tmp_path)) is None
+    assert bench.stored_traffic("w", "conv2", conv2, TUNE, prof_dir=str(tmp_path / "missing")) is None
+
+
 def test_committed_records_carry_their_tuning_table():
     for name in os.listdir(os.path.join(ROOT, "profiles")):
         if name.startswith("traffic_") and name.endswith(".json"):
