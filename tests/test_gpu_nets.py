@@ -107,7 +107,7 @@ def kernel_timed_pass(model, xd, nl):
     return y, starts, stops
 
 
-@pytest.mark.parametrize("name,batch", [("cifar_quick", 32), ("alexnet", 16)])
+@pytest.mark.parametrize("name,batch", [("cifar_quick", 32), ("alexnet", 16), ("alexnet", 1)])
 def test_kernel_timed_forward_matches_and_orders_spans(gpu, name, batch):
     """cnn_net_fwd_kernel_timed: the same output as the untimed pass; every
     layer's span is non-negative, and the span of a layer with kernels ends
