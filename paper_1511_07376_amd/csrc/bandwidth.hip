@@ -106,20 +106,6 @@ __global__ void __launch_bounds__(kThreads) maxpool_f32(PoolParams p) {
     run_fills(p.fills);
 }
 
-// Division by a runtime constant through a multiply-high (exact for n < 2^31):
-// the unsigned method of Granlund and Montgomery, "Division by invariant
-// integers using multiplication" (PLDI 1994), with l = ceil(log2 d) and
-// m = floor(2^32 (2^l - d) / d) + 1, so that n / d = (mulhi(m, n) + n) >> l.
-struct FastDiv {
-    unsigned d, m, l;
-};
-FastDiv make_fastdiv(unsigned d) {
-    unsigned l = 0;
-    while ((1u << l) < d) ++l;
-    const uint64_t m = ((((uint64_t)1 << l) - d) << 32) / d + 1;
-    return FastDiv{d, (unsigned)m, l};
-}
-__device__ inline unsigned fdiv(unsigned n, FastDiv f) { return (__umulhi(f.m, n) + n) >> f.l; }
 
 // Pooling with the input staged in LDS: a workgroup takes a run of whole
 // (n, c) planes, which is one contiguous stretch of memory, reads it with

@@ -53,6 +53,23 @@ class SpanPause {
     KernelSpan* saved_;
 };
 
+// Division by a runtime constant through a multiply-high (exact for n < 2^31):
+// the unsigned method of Granlund and Montgomery, "Division by invariant
+// integers using multiplication" (PLDI 1994), with l = ceil(log2 d) and
+// m = floor(2^32 (2^l - d) / d) + 1, so that n / d = (mulhi(m, n) + n) >> l.
+// A divisor of 0 is taken as 1 (only for launches that do no work).
+struct FastDiv {
+    unsigned d, m, l;
+};
+inline FastDiv make_fastdiv(unsigned d) {
+    if (d == 0) d = 1;
+    unsigned l = 0;
+    while ((1u << l) < d) ++l;
+    const uint64_t m = ((((uint64_t)1 << l) - d) << 32) / d + 1;
+    return FastDiv{d, (unsigned)m, l};
+}
+__device__ inline unsigned fdiv(unsigned n, FastDiv f) { return (__umulhi(f.m, n) + n) >> f.l; }
+
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 

@@ -95,6 +95,10 @@ int conv_prepare(const ConvShape& s, int* cfg, ConvParams* out, int* per_launch)
     prm.Kr = prm.Cg * prm.RS;
     prm.HW = s.H * s.W;
     prm.PQ = s.P * s.Q;
+    prm.f_rs = make_fastdiv(prm.RS);
+    prm.f_s = make_fastdiv(s.S);
+    prm.f_pq = make_fastdiv(prm.PQ);
+    prm.f_q = make_fastdiv(s.Q);
     prm.G = s.G;
     prm.splits = 1;
     prm.kchunk = prm.Kr;

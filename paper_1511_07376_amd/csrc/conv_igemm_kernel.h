@@ -63,6 +63,7 @@ struct ConvParams {
     int G;       // groups (grid z = G * splits)
     int splits;  // reduction chunks; > 1: partial tiles are added atomically
     int kchunk;  // taps per chunk (a multiple of every slab length; Kr if splits == 1)
+    FastDiv f_rs, f_s, f_pq, f_q;  // division by R*S, S, P*Q and Q
 };
 
 // Gather modes.
@@ -164,9 +165,9 @@ conv2d_igemm_f32(ConvParams p) {
     const int m = m0 + mloc;
     int hb, wb, lane_off;
     if (m < p.M) {
-        const int n = m / p.PQ;
+        const int n = (int)fdiv(m, p.f_pq);
         const int pq = m - n * p.PQ;
-        const int pp = pq / p.Q;
+        const int pp = (int)fdiv(pq, p.f_q);
         const int qq = pq - pp * p.Q;
         hb = pp * p.sh - p.ph;
         wb = qq * p.sw - p.pw;
@@ -187,9 +188,9 @@ conv2d_igemm_f32(ConvParams p) {
         for (int kk = threadIdx.x; kk < (niter + ST) * KS * BK; kk += NTB) {
             int e = GATHER == kGatherMask ? 31 : GATHER == kGatherStridedMask ? 63 : (int)0x80000000u;
             if (kk < klen) {
-                const int c = (kbeg + kk) / p.RS;
+                const int c = (int)fdiv(kbeg + kk, p.f_rs);
                 const int rs = kbeg + kk - c * p.RS;
-                const int r = rs / p.S;
+                const int r = (int)fdiv(rs, p.f_s);
                 const int s = rs - r * p.S;
                 const int toff = ((c * p.H + r) * p.W + s) * 4;
                 e = GATHER == kGatherMask ? ((toff << 5) | rs) : GATHER == kGatherStridedMask ? ((toff << 6) | rs) : toff;
@@ -219,9 +220,9 @@ conv2d_igemm_f32(ConvParams p) {
             const int mm = m0 + wpix + pi * 16;
             inv64[GATHER == kGatherStridedMask ? pi : 0] = ~0ull;
             if (mm < p.M) {
-                const int n = mm / p.PQ;
+                const int n = (int)fdiv(mm, p.f_pq);
                 const int pq = mm - n * p.PQ;
-                const int pp = pq / p.Q;
+                const int pp = (int)fdiv(pq, p.f_q);
                 const int qq = pq - pp * p.Q;
                 const int h0 = pp * p.sh - p.ph, w0 = qq * p.sw - p.pw;
                 soff[pi] = ((n * p.C + g * p.Cg) * p.HW + h0 * p.W + w0) * 4;
@@ -277,9 +278,9 @@ conv2d_igemm_f32(ConvParams p) {
             return;
         }
         const int ka0 = kbeg + kk0;  // absolute tap index
-        int c = ka0 / p.RS;
+        int c = (int)fdiv(ka0, p.f_rs);
         const int rs = ka0 - c * p.RS;
-        int r = rs / p.S;
+        int r = (int)fdiv(rs, p.f_s);
         int s = rs - r * p.S;
         int toff = ((c * p.H + r) * p.W + s) * 4;  // byte offset of tap (c, r, s)
 #pragma unroll
@@ -512,7 +513,7 @@ conv2d_igemm_f32(ConvParams p) {
     for (int j = 0; j < FN; ++j) {
         const int mc = m0 + wn * FN * 32 + j * 32 + l32;
         mok[j] = mc < p.M;
-        const int n = mok[j] ? mc / p.PQ : 0;
+        const int n = mok[j] ? (int)fdiv(mc, p.f_pq) : 0;
         const int pq = mok[j] ? mc - n * p.PQ : 0;
         yb[j] = p.y + n * p.K * p.PQ + pq;
     }
