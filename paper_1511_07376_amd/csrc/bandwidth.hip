@@ -367,12 +367,17 @@ __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
     for (int it = threadIdx.x; it < plane; it += kThreads) {
         const int pix = row0 * p.W + it;
         const int lane_off = (unsigned)pix < (unsigned)HW ? pix * 4 : (int)0x80000000u;
+        // The channel's part of the offset is uniform and goes in the load's
+        // scalar offset.  For a channel outside the tensor it is 0x7fffffff:
+        // with the lane's part below 2^32 - 2^31 + 1 (a pixel offset, or 2^31
+        // for a pixel outside the image) the sum stays below 2^32 and at or
+        // past the resource's 0x7fffffff bytes, so the load reads 0.
         float v[NV];
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
             const int c = cs + j;  // uniform
-            const int off = (unsigned)c < (unsigned)p.C ? lane_off + c * hw4 : (int)0x80000000u;
-            v[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0));
+            const int soff = (unsigned)c < (unsigned)p.C ? c * hw4 : 0x7fffffff;
+            v[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(xres, lane_off, soff, 0));
         }
         if (p.relu_x) {  // uniform
 #pragma unroll
