@@ -368,10 +368,11 @@ __global__ void __launch_bounds__(kThreads) lrn_pool_f32(LrnPoolParams p) {
         const int pix = row0 * p.W + it;
         const int lane_off = (unsigned)pix < (unsigned)HW ? pix * 4 : (int)0x80000000u;
         // The channel's part of the offset is uniform and goes in the load's
-        // scalar offset.  For a channel outside the tensor it is 0x7fffffff:
-        // with the lane's part below 2^32 - 2^31 + 1 (a pixel offset, or 2^31
-        // for a pixel outside the image) the sum stays below 2^32 and at or
-        // past the resource's 0x7fffffff bytes, so the load reads 0.
+        // scalar offset; for a channel outside the tensor it is 0x7fffffff.
+        // The lane's part is at most 2^31 (a pixel offset, or 2^31 for a pixel
+        // outside the image), so the sum of the two stays below 2^32, and it
+        // reaches the resource's 0x7fffffff bytes, and reads 0, whenever
+        // either part is out of range.
         float v[NV];
 #pragma unroll
         for (int j = 0; j < NV; ++j) {

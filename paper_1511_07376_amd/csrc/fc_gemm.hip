@@ -14,9 +14,10 @@
 // stored to LDS).  The LDS round trip of a slab (store, barrier, fragment
 // reads) overlaps the matrix-core work of the slab before it: a wave holds
 // two sets of fragment registers, and the barrier that publishes slab s + 1
-// sits inside slab s's matrix-core instructions.  The loads go through buffer resources: an index past the matrix gets
-// an out-of-range offset that reads 0, so the loads carry no branches and the
-// compiler can wait for exactly the slab it needs rather than for all of them.
+// sits inside slab s's matrix-core instructions.  The loads go through buffer
+// resources: an index past the matrix gets an out-of-range offset that reads
+// 0, so the loads carry no branches and the compiler can wait for exactly the
+// slab it needs rather than for all of them.
 //
 // A batch of 1 to 256 images gives few output tiles, far fewer than the
 // chip's 256 compute units, so the reduction is split across workgroups
