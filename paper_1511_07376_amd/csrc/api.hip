@@ -411,9 +411,9 @@ int run_net(const cnn_layer_desc* L, int n, const float* x, int N, int C, int H,
             if (!p.split || p.skipped) continue;
             if (first_split < 0) first_split = i;
             float* dst = i == last ? y : reinterpret_cast<float*>(split_area + p.split_off);
-            fills.push_back(BiasFill{dst, L[i].bias, N, p.outC, p.outH * p.outW});
+            fills.push_back(make_bias_fill(dst, L[i].bias, N, p.outC, p.outH * p.outW));
         }
-        if (!fills.empty() && (int)fills.size() <= kMaxBiasFills) {
+        if (!fills.empty() && (int)fills.size() <= kMaxPoolFills) {
             int h = first_split - 1;
             while (h >= 0 && plan[h].skipped) --h;
             if (h >= 0 && plan[h].type == CNN_LAYER_POOL) {

@@ -59,14 +59,14 @@ class SpanPause {
 // m = floor(2^32 (2^l - d) / d) + 1, so that n / d = (mulhi(m, n) + n) >> l.
 // A divisor of 0 is taken as 1 (only for launches that do no work).
 struct FastDiv {
-    unsigned d, m, l;
+    unsigned m, l;
 };
 inline FastDiv make_fastdiv(unsigned d) {
     if (d == 0) d = 1;
     unsigned l = 0;
     while ((1u << l) < d) ++l;
     const uint64_t m = ((((uint64_t)1 << l) - d) << 32) / d + 1;
-    return FastDiv{d, (unsigned)m, l};
+    return FastDiv{(unsigned)m, l};
 }
 __device__ inline unsigned fdiv(unsigned n, FastDiv f) { return (__umulhi(f.m, n) + n) >> f.l; }
 
@@ -143,20 +143,32 @@ int fc_splits(int N, int I, int O);
 // (FC: inner = 1; conv NCHW: inner = P*Q), in one launch per kMaxBiasFills
 // jobs.
 constexpr int kMaxBiasFills = 8;
+// A pooling kernel carries at most this many, so that its parameter block
+// stays within the size it had before the fills were added (a block 190 bytes
+// larger made the LRN + pooling kernels of AlexNet at batch 64 0.5 us slower
+// each, fills or not).  AlexNet at batch 16 has 6 split layers.
+constexpr int kMaxPoolFills = 6;
 struct BiasFill {
     float* y;
     const float* bias;
-    int N, O, inner;
+    int total;             // N * O * inner elements, below 2^31
+    int O;
+    FastDiv f_inner, f_o;  // division by inner and by O
 };
+inline BiasFill make_bias_fill(float* y, const float* bias, int N, int O, int inner) {
+    return BiasFill{y, bias, N * O * inner, O, make_fastdiv(inner), make_fastdiv(O)};
+}
 int launch_bias_fills(const BiasFill* jobs, int n, hipStream_t st);
-// Up to kMaxBiasFills of them, as a kernel argument: bias_fill_multi runs
-// them on their own, and a pooling kernel runs them after its own work
-// (fills argument of launch_pool / launch_lrn_pool), which saves the network
-// executor a launch.
-struct FillJobs {
-    BiasFill job[kMaxBiasFills];
+// Up to CAP of them, as a kernel argument: bias_fill_multi runs up to
+// kMaxBiasFills on their own, and a pooling kernel up to kMaxPoolFills after
+// its own work (fills argument of launch_pool / launch_lrn_pool), which saves
+// the network executor a launch.
+template <int CAP>
+struct FillJobsOf {
+    BiasFill job[CAP];
     int n;
 };
+using FillJobs = FillJobsOf<kMaxPoolFills>;
 // relu_x (pooling, LRN): take the input through a ReLU as it is read.
 // fills: bias fills the kernel also performs (NULL: none).
 int launch_pool(const PoolShape& s, int mode, int relu, const float* x, float* y, int32_t* idx,

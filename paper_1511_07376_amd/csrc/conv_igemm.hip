@@ -58,14 +58,6 @@ void choose_splits(ConvParams& p, const ConvConfig& c) {
     p.splits = splits > 1 ? ceil_div(p.Kr, p.kchunk) : 1;
 }
 
-// y[n][k][pq] = bias[k] (or 0): the starting value of a split reduction.
-__global__ void conv_fill_bias(float* __restrict__ y, const float* __restrict__ bias, int K, int PQ,
-                               int64_t total) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-         i += (int64_t)gridDim.x * blockDim.x)
-        y[i] = bias ? bias[(i / PQ) % K] : 0.0f;
-}
-
 }  // namespace
 }  // namespace conv
 
@@ -142,10 +134,9 @@ int launch_conv2d(const ConvShape& s, const float* x, const float* w, const floa
     const bool vec_w = (prm.Kr % 4 == 0) && ((reinterpret_cast<uintptr_t>(w) & 15) == 0);
     const int64_t img = (int64_t)s.C * prm.HW;
     const int64_t total = (int64_t)s.N * s.K * prm.PQ;
-    if (prm.splits > 1 && !(opt && opt->prefilled)) {
-        enqueue(conv::conv_fill_bias, dim3((unsigned)std::min<int64_t>(ceil_div64(total, 256), 4096)),
-                           dim3(256), 0, st, y, bias, s.K, prm.PQ, total);
-        rc = check_launch("conv_fill_bias");
+    if (prm.splits > 1 && !(opt && opt->prefilled)) {  // y[n][k][pq] = bias[k]: the sums' start
+        const BiasFill fill = make_bias_fill(y, bias, s.N, s.K, prm.PQ);
+        rc = launch_bias_fills(&fill, 1, st);
         if (rc != CNN_OK) return rc;
     }
     for (int n0 = 0; n0 < s.N; n0 += per_launch) {

@@ -244,10 +244,9 @@ fc_gemm_f32(FcParams p) {
 }
 
 // y[n][o] = bias[o] (or 0): the starting value of the split-reduction sums.
-__global__ void fc_fill_bias(float* y, const float* bias, int N, int O) {
-    const int64_t total = (int64_t)N * O;
-    for (int64_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x)
-        y[i] = bias ? bias[i % O] : 0.0f;
+int fill_fc_bias(const FcParams& prm, hipStream_t st) {
+    const BiasFill fill = make_bias_fill(prm.y, prm.bias, prm.N, prm.O, 1);
+    return launch_bias_fills(&fill, 1, st);
 }
 
 // Batches of at most 64 images (NB blocks of 32): each wave owns OB blocks of
@@ -461,7 +460,7 @@ int launch_fc_gemv(const FcParams& prm, bool vec, bool relu_in, hipStream_t st) 
 }
 
 // Several outputs at once (FillJobs).
-__global__ void bias_fill_multi(FillJobs f) { run_fills(f); }
+__global__ void bias_fill_multi(FillJobsOf<kMaxBiasFills> f) { run_fills(f); }
 
 // Tile and reduction split of an FC layer (one rule for launch_fc and the
 // network planner).
@@ -503,10 +502,10 @@ int launch_fc_cfg(const FcParams& prm0, const FcGeom& g, hipStream_t st, bool* r
     dim3 grid(ceil_div(prm.O, TN), ceil_div(prm.N, TM), splits);
     dim3 block(64 * WMW * WNW);
     if (splits > 1) {
-        const int total = prm.N * prm.O;
-        if (!prefilled)
-            enqueue(fc_fill_bias, dim3(std::min(ceil_div(total, 256), 2048)), dim3(256), 0, st,
-                               prm.y, prm.bias, prm.N, prm.O);
+        if (!prefilled) {
+            const int rc = fill_fc_bias(prm, st);
+            if (rc != CNN_OK) return rc;
+        }
         enqueue((fc_gemm_f32<WMW, WNW, FM, FN, BK, D, VEC, true, RELU_X>), grid, block, 0, st, prm);
         int rc = check_launch("fc_gemm_f32");
         if (rc != CNN_OK) return rc;
@@ -540,9 +539,8 @@ int launch_fc_direct_t(const FcParams& prm0, hipStream_t st, bool* relu_left, bo
     const int splits = fc_direct_split(FcDirectGeom{OB, KW}, prm.I, prm.O, &prm.kchunk);
     const dim3 grid(ceil_div(prm.O, 32 * OB), splits), block(64 * KW);
     if (splits > 1 && !prefilled) {
-        const int total = prm.N * prm.O;
-        enqueue(fc_fill_bias, dim3(std::min(ceil_div(total, 256), 2048)), dim3(256), 0, st,
-                           prm.y, prm.bias, prm.N, prm.O);
+        const int rc = fill_fc_bias(prm, st);
+        if (rc != CNN_OK) return rc;
     }
     enqueue((fc_direct_f32<NB, OB, KW, RELU_X>), grid, block, 0, st, prm);
     int rc = check_launch("fc_direct_f32");
@@ -622,12 +620,12 @@ int fc_splits(int N, int I, int O) {
 
 int launch_bias_fills(const BiasFill* jobs, int n, hipStream_t st) {
     for (int j0 = 0; j0 < n; j0 += kMaxBiasFills) {
-        FillJobs f;
+        FillJobsOf<kMaxBiasFills> f;
         f.n = std::min(kMaxBiasFills, n - j0);
         int64_t most = 0;
         for (int j = 0; j < f.n; ++j) {
             f.job[j] = jobs[j0 + j];
-            most = std::max(most, (int64_t)f.job[j].N * f.job[j].O * f.job[j].inner);
+            most = std::max(most, (int64_t)f.job[j].total);
         }
         if (most == 0) continue;
         enqueue(bias_fill_multi, dim3((unsigned)std::min<int64_t>(ceil_div64(most, 256), 2048)),
