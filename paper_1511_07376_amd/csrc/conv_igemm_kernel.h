@@ -110,9 +110,13 @@ __device__ inline T outside_taps(int h0, int w0, int H, int W, int R, int S) {
 // output tile; their partial tiles are summed through LDS before the
 // epilogue.  This gives small-pixel-count layers more waves without
 // shrinking each wave's tile.
+// The strided gathers ask the compiler for four waves per SIMD (at most 128
+// registers a wave) where the tile allows it: up to three 32x32 accumulator
+// blocks with 16-tap slabs, or one with 32-tap slabs; larger strided tiles
+// cannot fit four and keep the compiler's default.
 template <int WMW, int WNW, int FM, int FN, int BK, bool VEC_W, int GATHER, int KS, int ST>
 __global__ void __launch_bounds__(64 * WMW * WNW * KS)
-__attribute__((amdgpu_waves_per_eu(GATHER == kGatherStrided && FM * FN <= 3 ? 4 : 1)))
+__attribute__((amdgpu_waves_per_eu(GATHER == kGatherStrided && FM * FN * BK <= 48 ? 4 : 1)))
 conv2d_igemm_f32(ConvParams p) {
     static_assert(ST % 2 == 0, "the two LDS buffers alternate within a round of ST slabs");
     constexpr int TM = WMW * FM * 32;  // output channels per workgroup

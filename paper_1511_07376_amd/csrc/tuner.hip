@@ -50,15 +50,16 @@ int tune(const ConvShape& s, const float* x, const float* w, const float* bias, 
     hipEvent_t e0, e1;
     if (hipEventCreate(&e0) != hipSuccess) return -1;
     if (hipEventCreate(&e1) != hipSuccess) {
-        hipEventDestroy(e0);
+        (void)hipEventDestroy(e0);
         return -1;
     }
     // ms per run of configuration c over `runs` back-to-back launches; < 0 on failure
     auto time_cfg = [&](int c, int runs) -> float {
         if (launch_conv2d(s, x, w, bias, relu, y, st, c) != CNN_OK) return -1.0f;  // warm-up run
-        hipEventRecord(e0, st);
-        for (int r = 0; r < runs; ++r) launch_conv2d(s, x, w, bias, relu, y, st, c);
-        hipEventRecord(e1, st);
+        if (hipEventRecord(e0, st) != hipSuccess) return -1.0f;
+        for (int r = 0; r < runs; ++r)
+            if (launch_conv2d(s, x, w, bias, relu, y, st, c) != CNN_OK) return -1.0f;
+        if (hipEventRecord(e1, st) != hipSuccess) return -1.0f;
         if (hipEventSynchronize(e1) != hipSuccess) return -1.0f;
         float ms = 0.0f;
         if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) return -1.0f;
@@ -84,8 +85,8 @@ int tune(const ConvShape& s, const float* x, const float* w, const float* bias, 
             top = best_ms[i];
             best = first[i].second;
         }
-    hipEventDestroy(e0);
-    hipEventDestroy(e1);
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
     (void)hipGetLastError();
     return best;
 }
