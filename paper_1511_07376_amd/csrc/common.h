@@ -114,6 +114,8 @@ int conv2d_num_configs();
 const char* conv2d_config_name(int i);
 // Reduction splits configuration cfg (-1: heuristic) uses for this shape.
 int conv2d_splits(const ConvShape& s, int cfg);
+// The built-in heuristic's configuration for this shape (-1 if none applies).
+int conv2d_heuristic_config(const ConvShape& s);
 // Convolution with the tuned configuration for this shape (auto-tuning it
 // first when auto-tuning is on and the shape is new).
 int conv2d_dispatch(const ConvShape& s, const float* x, const float* w, const float* bias,

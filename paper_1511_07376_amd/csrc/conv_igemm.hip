@@ -112,6 +112,12 @@ int conv_prepare(const ConvShape& s, int* cfg, ConvParams* out, int* per_launch)
 
 }  // namespace
 
+int conv2d_heuristic_config(const ConvShape& s) {
+    ConvParams prm;
+    int per_launch, cfg = -1;
+    return conv_prepare(s, &cfg, &prm, &per_launch) == CNN_OK ? cfg : -1;
+}
+
 int conv2d_splits(const ConvShape& s, int cfg) {
     ConvParams prm;
     int per_launch;

@@ -469,11 +469,11 @@ struct FcGeom {
     int target;        // workgroups to aim for (two to four per compute unit)
 };
 
-// tm: 32 (launch_fc_cfg<1, 4, 1, 1, 32, 4>) or 64 (launch_fc_cfg<2, 2, 1, 1, 16, 4>);
-// target in workgroups for a batch of N.
-FcGeom fc_geom(int tm, int N) {
+// tm: 32 (launch_fc_cfg<1, 4, 1, 1, 32, 4>) or 64 (launch_fc_cfg<2, 2, 1, 1, bk, 4>,
+// bk 16 or 32); target in workgroups for a batch of N.
+FcGeom fc_geom(int tm, int N, int bk = 16) {
     if (tm == 32) return FcGeom{32, 128, 4 * 32, 512};
-    return FcGeom{64, 64, 4 * 16, N <= 64 ? 512 : 1024};
+    return FcGeom{64, 64, 4 * bk, N <= 64 ? 512 : 1024};
 }
 
 // Splits and the reduction length per split.
@@ -572,6 +572,7 @@ const FcConfig kFcConfigs[] = {
     {"tiled, 32 images x 128 features, 1x4 waves, 32-tap slabs", 1 << 30, false},
     {"direct, 32 features per wave, 8 waves", 64, true},
     {"matrix-vector", kGemvMaxN, false},
+    {"tiled, 64 images x 64 features, 2x2 waves, 32-tap slabs", 1 << 30, false},
 };
 constexpr int kNumFcConfigs = sizeof(kFcConfigs) / sizeof(kFcConfigs[0]);
 
@@ -589,9 +590,14 @@ constexpr int kNumFcConfigs = sizeof(kFcConfigs) / sizeof(kFcConfigs[0]);
 // (fc6 64.0 against 50.0 us).  In the network at batch 16, with the input's
 // ReLU deferred from the layer before, fc7 (4096 -> 4096) took 21.4 us direct
 // against 20.2 tiled.  Above 64 images, layers of at most 1024 features run
-// 3-45% faster on the 32 x 128 tiles (twice the row tiles of 64 x 64).
+// 3-45% faster on the 32 x 128 tiles (twice the row tiles of 64 x 64).  At
+// 33-64 images the wide layers take 32-tap slabs on the 64 x 64 tiles (the
+// same split count, twice the matrix-core work per barrier): AlexNet's fc6
+// at batch 64 went from 45 to 43 us in the network; fc8 keeps 16-tap slabs,
+// whose finer split granule gives it twice the splits.
 int fc_heuristic(int N, int I, int O, bool vec) {
     if (N <= kGemvMaxN) return 3;
+    if (N > 32 && N <= 64 && O >= 2048 && I >= 4096) return 4;
     if (vec && N <= 64 && I <= 4096 && O <= (N <= 32 ? 2048 : 512)) return 2;
     if (N <= 32) return 1;
     if (N > 64 && O <= 1024 && I >= 256) return 1;
@@ -604,6 +610,7 @@ int fc_config_splits(int cfg, int N, int I, int O) {
         case 0: return fc_split(fc_geom(64, N), N, I, O, &kchunk);
         case 1: return fc_split(fc_geom(32, N), N, I, O, &kchunk);
         case 2: return fc_direct_split(FcDirectGeom{1, 8}, I, O, &kchunk);
+        case 4: return fc_split(fc_geom(64, N, 32), N, I, O, &kchunk);
         default: return 1;
     }
 }
@@ -674,6 +681,7 @@ int launch_fc(const float* x, int N, int I, const float* w, const float* bias, i
         case 0: return CNN_FC_CFG(fc_geom(64, N), 2, 2, 1, 1, 16, 4);  // 64 x 64
         case 1: return CNN_FC_CFG(fc_geom(32, N), 1, 4, 1, 1, 32, 4);  // 32 images x 128 features
         case 2: return launch_fc_direct<1, 8>(prm, relu_in, st, relu_left, prefilled);
+        case 4: return CNN_FC_CFG(fc_geom(64, N, 32), 2, 2, 1, 1, 32, 4);  // 64 x 64, 32-tap slabs
         default:
             static_assert(kGemvMaxN == 2, "one instantiation per batch size");
             return N == 1 ? launch_fc_gemv<1>(prm, vec, relu_in, st) : launch_fc_gemv<2>(prm, vec, relu_in, st);
